@@ -1,0 +1,207 @@
+"""The KVGov hot path, computed plainly on the CPU.  TEST INFRASTRUCTURE ONLY.
+
+Readings of the paper taken here (each also listed in the design notes):
+
+* Salt (Sec. 4.1, first display): sigma_p = HMAC-SHA256 with key K (the
+  server secret) over the principal id bytes; the full 32-byte output.
+* Token bytes: a block of B = 16 tokens is the 64 bytes of its int32 ids in
+  little-endian order, nothing else (the paper does not fix an encoding).
+* H is SHA-256 and "H(x, y)" is the concatenation x || y, parent digest
+  first, as raw 32 bytes (Sec. 2.1 display; Sec. 4.1 names SHA256).
+* Unsalted root: h_0 = SHA256(T_0) with no seed (Sec. 2.1 display).
+* Root salting: h_0 = SHA256(sigma_p || T_0), later blocks chained
+  unchanged (Sec. 4.1 display).
+* Boundary salting (Sec. 4.2 display): blocks j < k unsalted,
+  h_k = SHA256(sigma_p || h_{k-1} || T_k), blocks after k chained.  k is
+  given per request as a token offset, k = boundary_tok // B (Sec. 5.6: a
+  divergence at token i invalidates every block from floor(i/B)); k = 0 has
+  no parent and is SHA256(sigma_p || T_0), the root-salted case; k at or
+  beyond the last full block salts nothing (Sec. 4.2, "all-or-nothing").
+* Only full blocks are hashed, inserted and probed; a trailing partial block
+  is ignored (Sec. 2.1: matches are truncated to a block boundary).
+* Lookup returns the index of the first block whose hash is not in the table
+  (the number of leading blocks matched, Table "tab:taxonomy"), and does not
+  change the table.  Insert is set union.
+"""
+from __future__ import annotations
+
+import hashlib
+import hmac
+import multiprocessing as mp
+import os
+import struct
+from typing import Iterable, List, Optional, Sequence
+
+import numpy as np
+
+NONE, ROOT, BOUNDARY = 0, 1, 2
+BLOCK = 16
+DIGEST = 32
+
+
+def sha256(data: bytes) -> bytes:
+    return hashlib.sha256(data).digest()
+
+
+# ---------------------------------------------------------------------------
+# a1: salts (Sec. 4.1)
+# ---------------------------------------------------------------------------
+
+def salt(K: bytes, principal_id: bytes) -> bytes:
+    """sigma_p = HMAC_K(principal_id) with SHA-256 (Sec. 4.1; abstract)."""
+    return hmac.new(bytes(K), bytes(principal_id), hashlib.sha256).digest()
+
+
+def salts(K: bytes, principal_ids) -> List[bytes]:
+    """One salt per row of ``principal_ids`` (uint8 [P, L] or a list of bytes)."""
+    return [salt(K, bytes(np.asarray(pid, dtype=np.uint8).tobytes())
+                 if not isinstance(pid, (bytes, bytearray)) else bytes(pid))
+            for pid in principal_ids]
+
+
+# ---------------------------------------------------------------------------
+# a2 / a3: chained block hashes (Sec. 2.1, 4.1, 4.2)
+# ---------------------------------------------------------------------------
+
+def block_bytes(tokens: Sequence[int], j: int) -> bytes:
+    """T_j: the 16 int32 token ids of block j, little-endian."""
+    return struct.pack("<16i", *[int(t) for t in tokens[BLOCK * j:BLOCK * (j + 1)]])
+
+
+def chain(tokens: Sequence[int], mode: int, salt_bytes: Optional[bytes] = None,
+          boundary_tok: Optional[int] = None, hash_fn=sha256) -> List[bytes]:
+    """Block hashes h_0 .. h_{n-1} of one request, n = len(tokens) // 16."""
+    n_full = len(tokens) // BLOCK
+    if mode == BOUNDARY:
+        if boundary_tok is None or not 0 <= boundary_tok <= len(tokens):
+            raise ValueError("boundary_tok outside [0, len]")
+        k = boundary_tok // BLOCK
+    elif mode in (NONE, ROOT):
+        k = None
+    else:
+        raise ValueError("unknown mode")
+    if mode != NONE and (salt_bytes is None or len(salt_bytes) != DIGEST):
+        raise ValueError("salted modes need a 32-byte salt")
+    out: List[bytes] = []
+    prev = b""  # h_{-1} does not exist
+    for j in range(n_full):
+        salted = (mode == ROOT and j == 0) or (mode == BOUNDARY and j == k)
+        msg = (salt_bytes if salted else b"") + prev + block_bytes(tokens, j)
+        prev = hash_fn(msg)
+        out.append(prev)
+    return out
+
+
+def _check_batch(tokens, tok_offsets, principal, P, mode, boundary_tok):
+    tok_offsets = np.asarray(tok_offsets, dtype=np.int64)
+    n = tok_offsets.shape[0] - 1
+    if n < 0 or np.any(np.diff(tok_offsets) < 0) or (n >= 0 and tok_offsets[0] < 0) \
+            or tok_offsets[-1] > len(tokens):
+        raise ValueError("bad offsets")
+    if mode != NONE:
+        principal = np.asarray(principal)
+        if principal.shape[0] != n or np.any(principal < 0) or np.any(principal >= P):
+            raise ValueError("bad principal")
+    return tok_offsets, n
+
+
+def hash_chains(tokens, tok_offsets, principal, salt_list, mode,
+                boundary_tok=None, requests: Optional[Iterable[int]] = None) -> np.ndarray:
+    """Chains of a ragged batch in the flat layout of the C ABI.
+
+    Returns uint8 [sum_r len_r // 16, 32], request after request.  With
+    ``requests`` given, only those requests are hashed (in that order)."""
+    tok_offsets, n = _check_batch(tokens, tok_offsets, principal, len(salt_list), mode,
+                                  boundary_tok)
+    rows = range(n) if requests is None else requests
+    out = []
+    for r in rows:
+        a, b = int(tok_offsets[r]), int(tok_offsets[r + 1])
+        s = salt_list[int(principal[r])] if mode != NONE else None
+        bt = int(boundary_tok[r]) if mode == BOUNDARY else None
+        out.extend(chain(tokens[a:b], mode, s, bt))
+    if not out:
+        return np.zeros((0, DIGEST), dtype=np.uint8)
+    return np.frombuffer(b"".join(out), dtype=np.uint8).reshape(-1, DIGEST)
+
+
+_POOL_ARGS = None
+
+
+def _pool_chunk(rng_):
+    tokens, tok_offsets, principal, salt_list, mode, boundary_tok = _POOL_ARGS
+    return hash_chains(tokens, tok_offsets, principal, salt_list, mode,
+                       boundary_tok, requests=range(*rng_)).tobytes()
+
+
+def hash_chains_parallel(tokens, tok_offsets, principal, salt_list, mode,
+                         boundary_tok=None, processes: Optional[int] = None,
+                         requests: Optional[Sequence[int]] = None) -> np.ndarray:
+    """``hash_chains`` split over worker processes by request ranges.
+
+    Same result, request order kept; ``requests`` (a contiguous range) limits
+    the work to those requests."""
+    global _POOL_ARGS
+    tok_offsets = np.asarray(tok_offsets, dtype=np.int64)
+    n = tok_offsets.shape[0] - 1
+    lo, hi = (0, n) if requests is None else (int(requests[0]), int(requests[-1]) + 1)
+    processes = processes or os.cpu_count() or 1
+    step = max(1, (hi - lo + 4 * processes - 1) // (4 * processes))
+    chunks = [(a, min(a + step, hi)) for a in range(lo, hi, step)]
+    _POOL_ARGS = (tokens, tok_offsets, principal, salt_list, mode, boundary_tok)
+    try:
+        ctx = mp.get_context("fork")
+        with ctx.Pool(processes) as pool:
+            parts = pool.map(_pool_chunk, chunks)
+    finally:
+        _POOL_ARGS = None
+    data = b"".join(parts)
+    return np.frombuffer(data, dtype=np.uint8).reshape(-1, DIGEST)
+
+
+# ---------------------------------------------------------------------------
+# a4 / a5: the block prefix cache (Sec. 2.1; Table "tab:taxonomy")
+# ---------------------------------------------------------------------------
+
+def _keys(hashes: np.ndarray, lo: int = 0, hi: Optional[int] = None) -> List[bytes]:
+    h = np.ascontiguousarray(hashes[lo:hi], dtype=np.uint8)
+    raw = h.tobytes()
+    return [raw[i:i + DIGEST] for i in range(0, len(raw), DIGEST)]
+
+
+class Table:
+    """The cache as a set of 32-byte keys.  No capacity limit, no eviction."""
+
+    def __init__(self):
+        self.keys = set()
+
+    def insert(self, hashes: np.ndarray, blk_offsets=None) -> int:
+        """T <- T u {every key of the batch}; returns how many were not in T."""
+        if blk_offsets is not None:
+            blk_offsets = np.asarray(blk_offsets, dtype=np.int64)
+            lo, hi = int(blk_offsets[0]), int(blk_offsets[-1])
+        else:
+            lo, hi = 0, int(hashes.shape[0])
+        new = set(_keys(hashes, lo, hi)) - self.keys
+        self.keys |= new
+        return len(new)
+
+    def lookup(self, hashes: np.ndarray, blk_offsets) -> np.ndarray:
+        """hit[r] = first j with h_j(r) not in T, or n_full(r) if none is missing."""
+        return lookup_hits(self.keys, hashes, blk_offsets)
+
+
+def lookup_hits(keys: set, hashes: np.ndarray, blk_offsets,
+                requests: Optional[Iterable[int]] = None) -> np.ndarray:
+    blk_offsets = np.asarray(blk_offsets, dtype=np.int64)
+    n = blk_offsets.shape[0] - 1
+    rows = list(range(n)) if requests is None else list(requests)
+    out = np.zeros(len(rows), dtype=np.int32)
+    raw = np.ascontiguousarray(hashes, dtype=np.uint8)
+    for i, r in enumerate(rows):
+        a, b = int(blk_offsets[r]), int(blk_offsets[r + 1])
+        j = 0
+        while j < b - a and raw[a + j].tobytes() in keys:
+            j += 1
+        out[i] = j
+    return out
