@@ -1,0 +1,215 @@
+/*
+ * kvgov.h -- C ABI of libkvgov: the data-parallel hot path of KVGov's
+ * HMAC-keyed namespace isolation for multi-tenant prefix caches, on AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The three steps of the path and the paper passages that define them:
+ *
+ *   salts        sigma_p = HMAC-SHA256(K, principal_id)         Sec. 4.1
+ *   hash_chains  h_0 = H(T_0), h_j = H(h_{j-1} || T_j), with    Sec. 2.1
+ *                the salt at the chain root (h_0 = H(sigma_p || T_0))   Sec. 4.1
+ *                or at the divergence boundary k                         Sec. 4.2
+ *                (h_k = H(sigma_p || h_{k-1} || T_k))
+ *   cache        insert block hashes; lookup returns, per       Sec. 2.1;
+ *                request, the number of leading blocks present  Table tab:taxonomy
+ *                (first miss), i.e. the longest cached prefix   (block prefix cache)
+ *
+ * H is SHA-256 (FIPS 180-4).  T_j is the 64 bytes of block j: 16 int32
+ * token ids, little-endian, back to back.  Only full blocks are hashed; a
+ * trailing partial block is ignored.  Digests are stored as their standard
+ * 32-byte big-endian serialisation.
+ *
+ * Conventions for every call:
+ *   - Array arguments marked "device" are device pointers owned by the
+ *     caller; the library never frees or keeps them.  "host" pointers are
+ *     read or written before the call returns.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Work is
+ *     enqueued on it in order; calls return without waiting unless stated.
+ *   - Every call returns KVGOV_OK (0) or a negative KVGOV_E_* code.
+ *     Argument errors that can be seen on the host return before anything is
+ *     enqueued and have no side effects.  Errors found by a kernel (bad
+ *     offsets, a principal or boundary out of range, a full table) are
+ *     latched: in the caller's `status` word for the hashing calls, in the
+ *     cache object for the cache calls, and reported by the next call that
+ *     waits for the stream.
+ *   - K and the salts are secrets: the library keeps no copy of K after
+ *     kvgov_salts returns and logs nothing.
+ *   - The calls allocate no device memory except kvgov_cache_create and the
+ *     stream-ordered scratch of kvgov_hash_chains (see there).
+ */
+#ifndef KVGOV_H
+#define KVGOV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Salt placement.  NONE: unsalted chain (Sec. 2.1).  ROOT: salt in the first
+ * block's message (Sec. 4.1).  BOUNDARY: salt in block k's message, blocks
+ * below k unsalted and shared across principals (Sec. 4.2). */
+#define KVGOV_NONE 0
+#define KVGOV_ROOT 1
+#define KVGOV_BOUNDARY 2
+
+#define KVGOV_BLOCK_SIZE 16 /* tokens per block; the only size supported */
+#define KVGOV_DIGEST_BYTES 32
+#define KVGOV_MAX_KEY_BYTES 64    /* HMAC keys up to one SHA-256 block */
+#define KVGOV_MAX_ID_BYTES 1024   /* principal id length limit */
+#define KVGOV_MIN_LOG2_SLOTS 4
+#define KVGOV_MAX_LOG2_SLOTS 31
+
+#define KVGOV_OK 0
+#define KVGOV_E_INVAL (-1)       /* bad argument seen on the host; nothing enqueued */
+#define KVGOV_E_UNSUPPORTED (-2) /* valid but not supported (block size, key length) */
+#define KVGOV_E_OFFSETS (-3)     /* kernel: offsets not monotone, out of bounds, or
+                                    blk_offsets not the prefix sum of len // 16 */
+#define KVGOV_E_BOUNDARY (-4)    /* kernel: boundary_tok outside [0, len] */
+#define KVGOV_E_PRINCIPAL (-5)   /* kernel: principal index outside [0, P) */
+#define KVGOV_E_FULL (-6)        /* kernel: no free slot for a new key */
+#define KVGOV_E_HIP (-7)         /* a HIP runtime call failed */
+#define KVGOV_E_NOMEM (-8)       /* device allocation failed */
+#define KVGOV_E_CAPACITY (-9)    /* export buffer smaller than the key count */
+#define KVGOV_E_DEVICE (-10)     /* cache used with another device current */
+#define KVGOV_E_INTERNAL (-11)   /* kernel: a bounded wait ran out (never expected) */
+
+/* Opaque, library-owned prefix-cache table on one device. */
+typedef struct kvgov_cache kvgov_cache;
+
+/* Message for an error code (static string; never NULL). */
+const char *kvgov_strerror(int code);
+
+/* ABI version, (major << 16) | minor. */
+int kvgov_version(void);
+
+/*
+ * a1 -- per-principal salts (Sec. 4.1): salts[p] = HMAC-SHA256(K, id_p).
+ *
+ * K            host, K_len bytes, 1 <= K_len <= 64 (RFC 2104 zero-pads K to
+ *              64 bytes; longer keys return KVGOV_E_UNSUPPORTED).
+ * principal_ids device, uint8 [P][id_len], row-major; id_len in [0, 1024].
+ * salts        device out, uint8 [P][32].
+ * Errors: KVGOV_E_INVAL (NULL pointer, P < 0, id_len out of range,
+ * K_len == 0), KVGOV_E_UNSUPPORTED (K_len > 64), KVGOV_E_HIP.
+ * P == 0 enqueues nothing.
+ */
+int kvgov_salts(const uint8_t *K, size_t K_len, const uint8_t *principal_ids,
+                int32_t id_len, int32_t P, uint8_t *salts, void *stream);
+
+/*
+ * Output layout helper: blk_offsets[r] = sum_{i<r} floor(len_i / block_size)
+ * with len_i = tok_offsets[i+1] - tok_offsets[i]; blk_offsets[0] = 0.
+ *
+ * tok_offsets  device, int64 [n + 1], non-decreasing.
+ * blk_offsets  device out, int64 [n + 1].
+ * status       device int32, zeroed by the caller; a negative length makes
+ *              the kernel store KVGOV_E_OFFSETS there (first error wins).
+ * Errors: KVGOV_E_INVAL, KVGOV_E_UNSUPPORTED (block_size != 16), KVGOV_E_HIP.
+ */
+int kvgov_block_offsets(const int64_t *tok_offsets, int32_t n, int32_t block_size,
+                        int64_t *blk_offsets, int32_t *status, void *stream);
+
+/*
+ * a2/a3 -- chained block hashes for a ragged batch (Sec. 2.1, 4.1, 4.2).
+ *
+ * tokens       device, int32 [n_tokens]; request r owns
+ *              tokens[tok_offsets[r] .. tok_offsets[r+1]).
+ * tok_offsets  device, int64 [n + 1]; 0 <= tok_offsets[r] <= tok_offsets[r+1]
+ *              <= n_tokens.
+ * principal    device, int32 [n], index into `salts`; unused (may be NULL)
+ *              for KVGOV_NONE.
+ * salts        device, uint8 [P][32] (from kvgov_salts); unused for NONE.
+ * mode         KVGOV_NONE, KVGOV_ROOT or KVGOV_BOUNDARY.
+ * boundary_tok device, int32 [n], BOUNDARY only (may be NULL otherwise):
+ *              the token offset of the divergence boundary, in [0, len_r];
+ *              the salted block is k = boundary_tok / 16.  k = 0 equals root
+ *              salting; k >= len_r / 16 salts no block (the unsalted chain).
+ * block_size   must be 16.
+ * blk_offsets  device, int64 [n + 1], as kvgov_block_offsets computes it.
+ * hashes       device out, uint8 [n_blocks][32]; request r's block j goes to
+ *              row blk_offsets[r] + j.  Rows of rejected requests are left
+ *              untouched.
+ * status       device int32, zeroed by the caller; kernels store the first
+ *              error (KVGOV_E_OFFSETS / _PRINCIPAL / _BOUNDARY) there and skip
+ *              the offending request.
+ * Scratch: for large batches the call orders requests longest first using
+ * 8 * n bytes from hipMallocAsync on `stream`, freed in stream order.
+ * Errors: KVGOV_E_INVAL, KVGOV_E_UNSUPPORTED, KVGOV_E_NOMEM, KVGOV_E_HIP.
+ */
+int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens,
+                      const int64_t *tok_offsets, int32_t n,
+                      const int32_t *principal, const uint8_t *salts, int32_t P,
+                      int32_t mode, const int32_t *boundary_tok, int32_t block_size,
+                      const int64_t *blk_offsets, uint8_t *hashes, int64_t n_blocks,
+                      int32_t *status, void *stream);
+
+/*
+ * a4/a5 -- the device-resident prefix-cache table (Sec. 2.1; Table
+ * tab:taxonomy, block prefix cache).  Open addressing over 2^log2_slots
+ * slots of 32-byte keys with full 256-bit compare; any 32-byte value is a
+ * valid key.  No eviction: a key stays until kvgov_cache_clear.
+ *
+ * create: allocates about 36 * 2^log2_slots bytes on the current device,
+ * cleared.  log2_slots in [4, 31].  Errors: KVGOV_E_INVAL, KVGOV_E_NOMEM,
+ * KVGOV_E_HIP.  The cache must be used with that device current
+ * (KVGOV_E_DEVICE otherwise).
+ */
+int kvgov_cache_create(int32_t log2_slots, kvgov_cache **out);
+
+/* Frees the table (waits for the device first).  NULL is accepted. */
+int kvgov_cache_destroy(kvgov_cache *c);
+
+/* Empties the table and its latched error, in stream order. */
+int kvgov_cache_clear(kvgov_cache *c, void *stream);
+
+/* Number of slots (host). */
+int kvgov_cache_slots(const kvgov_cache *c, int64_t *slots);
+
+/*
+ * T <- T u {hashes[blk_offsets[0] .. blk_offsets[n])}.  Duplicate keys in the
+ * batch and keys already present count once.
+ *
+ * hashes       device, uint8 [n_blocks][32].
+ * blk_offsets  device, int64 [n + 1], non-decreasing, blk_offsets[n] <= n_blocks.
+ * n_new        host out or NULL.  Non-NULL: the call waits for `stream` and
+ *              stores the number of keys the batch added; it then returns
+ *              any latched error.  NULL: nothing waits.
+ * Kernel errors: KVGOV_E_OFFSETS (nothing inserted), KVGOV_E_FULL (the table
+ * holds a consistent subset of the union; clear it before reuse).
+ */
+int kvgov_cache_insert(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,
+                       int32_t n, int64_t n_blocks, int64_t *n_new, void *stream);
+
+/*
+ * hit_blocks[r] = the first j < len_r/16 whose key hashes[blk_offsets[r] + j]
+ * is not in T, or blk_offsets[r+1] - blk_offsets[r] if every key is present.
+ * Reads the table only; sees every insert enqueued before it.
+ *
+ * hit_blocks   device out, int32 [n].
+ * Kernel errors: KVGOV_E_OFFSETS (latched; the affected rows are set to 0).
+ */
+int kvgov_cache_lookup(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,
+                       int32_t n, int64_t n_blocks, int32_t *hit_blocks, void *stream);
+
+/* Waits for `stream`; stores the number of keys in T and returns the latched
+ * error, if any. */
+int kvgov_cache_count(kvgov_cache *c, int64_t *n_keys, void *stream);
+
+/*
+ * Copies every key in T, in no particular order, to keys (device,
+ * uint8 [cap][32]); waits for `stream`; *n_keys = number of keys in T.
+ * Returns KVGOV_E_CAPACITY if that exceeds cap (the first cap keys found
+ * are written).  A latched error is not returned here (kvgov_cache_count
+ * returns it), so the keys of a table that reported KVGOV_E_FULL can still
+ * be read.
+ */
+int kvgov_cache_export(kvgov_cache *c, uint8_t *keys, int64_t cap, int64_t *n_keys,
+                       void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVGOV_H */

@@ -1,0 +1,468 @@
+// Device-resident prefix-cache table: batched insert and first-miss lookup.
+//
+// Paper: a block prefix cache keys KV blocks by their chained block hash and
+// resolves a request to the longest cached prefix, quantised to blocks; the
+// prober learns the number of leading blocks matched (Sec. 2.1; Table
+// tab:taxonomy, block prefix cache row).
+//
+// Layout (HBM):
+//   keys [slots][32 B]  the stored keys; an empty slot holds 32 bytes 0xFF.
+//                       Lookups read only this array: a probe is one 32-byte
+//                       read, and four consecutive slots share a 128-byte line,
+//                       so linear probing mostly stays in one line.
+//   tags [slots] u64    0 = empty, else (epoch << 32) | (claimant + 1): the
+//                       insert call that claimed the slot and the index of the
+//                       claiming key within that call's input.
+//   meta                key count, per-call counters, latched error, and the
+//                       presence bit of the all-0xFF key, which cannot live in
+//                       a slot because it is the empty pattern.
+//
+// Insert protocol (no fences, no waiting on other lanes).  A key walks its
+// probe sequence; at each slot it reads the tag:
+//   * empty          -> CAS the tag to (epoch, me); the winner writes the key
+//                       into the slot and counts one new key.
+//   * earlier epoch  -> the slot's key was written by an earlier kernel and is
+//                       visible: compare all 256 bits.
+//   * current epoch  -> the slot was claimed in this call; its key may not be
+//                       written yet, so compare against the claimant's key in
+//                       this call's input array instead.
+// Equal -> already present, stop.  Otherwise move to the next slot.  Two
+// copies of one key follow the same sequence and each slot changes state at
+// most once, so exactly one copy claims a slot and the other finds it.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <new>
+
+#include "common.h"
+
+namespace kvgov {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4), aligned(4)));
+
+struct CacheMeta {
+  unsigned long long n_keys;      // keys in the table (all-0xFF key included)
+  unsigned long long last_new;    // keys added by the latest insert
+  unsigned long long exported;    // keys written by the latest export
+  int32_t status;                 // latched error (0 = none)
+  int32_t ones_present;           // the all-0xFF key is in the table
+  int32_t call_bad;               // the current call was rejected by a kernel
+  int32_t pad_;
+};
+
+struct TableView {
+  u32x4 *keys;  // 2 per slot
+  unsigned long long *tags;
+  CacheMeta *meta;
+  uint64_t mask;  // slots - 1
+};
+
+struct Key {
+  u32x4 lo, hi;
+};
+
+__device__ __forceinline__ Key load_key(const uint8_t *p) {
+  const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
+  return Key{q[0], q[1]};
+}
+
+__device__ __forceinline__ bool key_eq(const Key &a, const Key &b) {
+  const uint32_t d = (a.lo.x ^ b.lo.x) | (a.lo.y ^ b.lo.y) | (a.lo.z ^ b.lo.z) |
+                     (a.lo.w ^ b.lo.w) | (a.hi.x ^ b.hi.x) | (a.hi.y ^ b.hi.y) |
+                     (a.hi.z ^ b.hi.z) | (a.hi.w ^ b.hi.w);
+  return d == 0;
+}
+
+__device__ __forceinline__ bool key_is_empty_pattern(const Key &a) {
+  return (a.lo.x & a.lo.y & a.lo.z & a.lo.w & a.hi.x & a.hi.y & a.hi.z & a.hi.w) ==
+         0xFFFFFFFFu;
+}
+
+// Slot index from all 256 bits (keys are digests, but any 32-byte value is
+// valid, so every word takes part), finished with a 64-bit mixer.
+__device__ __forceinline__ uint64_t slot_hash(const Key &k) {
+  uint64_t x = ((uint64_t)k.lo.y << 32 | k.lo.x) ^
+               (((uint64_t)k.lo.w << 32 | k.lo.z) * 0x9E3779B97F4A7C15ull) ^
+               (((uint64_t)k.hi.y << 32 | k.hi.x) * 0xC2B2AE3D27D4EB4Full) ^
+               (((uint64_t)k.hi.w << 32 | k.hi.z) * 0x165667B19E3779F9ull);
+  x ^= x >> 31;
+  x *= 0xBF58476D1CE4E5B9ull;
+  x ^= x >> 29;
+  return x;
+}
+
+// ---------------------------------------------------------------------------
+// kernels
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long long *tags,
+                                                    int64_t slots) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  const u32x4 ones = u32x4{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+  for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < slots; s += stride) {
+    keys[2 * s] = ones;
+    keys[2 * s + 1] = ones;
+    tags[s] = 0;
+  }
+}
+
+__global__ void k_meta_reset(CacheMeta *m) {
+  m->n_keys = 0;
+  m->last_new = 0;
+  m->exported = 0;
+  m->status = 0;
+  m->ones_present = 0;
+  m->call_bad = 0;
+}
+
+// Start of an insert: zero the per-call counter and check the key range.
+__global__ void k_insert_begin(CacheMeta *m, const int64_t *blk_offsets, int32_t n,
+                               int64_t n_blocks) {
+  m->last_new = 0;
+  const int64_t lo = blk_offsets[0], hi = blk_offsets[n];
+  const bool bad = lo < 0 || hi < lo || hi > n_blocks || hi - lo >= 0xFFFFFFFFll;
+  m->call_bad = bad ? 1 : 0;
+  if (bad) atomicCAS(&m->status, 0, KVGOV_E_OFFSETS);
+}
+
+__device__ __forceinline__ void add_wave_count(unsigned long long *dst1,
+                                               unsigned long long *dst2, uint32_t v) {
+  // one atomic per wave: sum over the active lanes
+  const uint64_t active = __ballot(1);
+  uint32_t s = v;
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) s += __shfl_xor(s, d, 64);
+  const int lane = threadIdx.x & 63;
+  if (lane == __builtin_ctzll(active) && s) {
+    atomicAdd(dst1, (unsigned long long)s);
+    if (dst2) atomicAdd(dst2, (unsigned long long)s);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hashes,
+                                                const int64_t *blk_offsets, int32_t n,
+                                                uint32_t epoch) {
+  if (__hip_atomic_load(&t.meta->call_bad, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+  const int64_t lo = blk_offsets[0], hi = blk_offsets[n];
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  const uint64_t slots = t.mask + 1;
+  uint32_t added = 0;
+  for (int64_t i = lo + (int64_t)blockIdx.x * 256 + threadIdx.x; i < hi; i += stride) {
+    const Key key = load_key(hashes + i * 32);
+    if (key_is_empty_pattern(key)) {
+      if (atomicExch(&t.meta->ones_present, 1) == 0) ++added;
+      continue;
+    }
+    const unsigned long long mine =
+        ((unsigned long long)epoch << 32) | (unsigned long long)(i - lo + 1);
+    uint64_t s = slot_hash(key) & t.mask;
+    uint64_t probes = 0;
+    while (true) {
+      unsigned long long tag =
+          __hip_atomic_load(&t.tags[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (tag == 0) {
+        unsigned long long expect = 0;
+        if (__hip_atomic_compare_exchange_strong(&t.tags[s], &expect, mine, __ATOMIC_RELAXED,
+                                                 __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT)) {
+          t.keys[2 * s] = key.lo;
+          t.keys[2 * s + 1] = key.hi;
+          ++added;
+          break;
+        }
+        tag = expect;  // somebody claimed it first: examine the claimant
+      }
+      Key other;
+      if ((uint32_t)(tag >> 32) == epoch) {
+        const int64_t c = (int64_t)(tag & 0xFFFFFFFFull) - 1;
+        other = load_key(hashes + (lo + c) * 32);
+      } else {
+        other = Key{t.keys[2 * s], t.keys[2 * s + 1]};
+      }
+      if (key_eq(key, other)) break;
+      s = (s + 1) & t.mask;
+      if (++probes >= slots) {
+        atomicCAS(&t.meta->status, 0, KVGOV_E_FULL);
+        break;
+      }
+    }
+  }
+  add_wave_count(&t.meta->last_new, &t.meta->n_keys, added);
+}
+
+// Is `key` in the table?  Reads the key array only.
+__device__ __forceinline__ bool probe(const TableView &t, const Key &key, bool ones_present) {
+  if (key_is_empty_pattern(key)) return ones_present;
+  uint64_t s = slot_hash(key) & t.mask;
+  for (uint64_t p = 0; p <= t.mask; ++p) {
+    const Key slot{t.keys[2 * s], t.keys[2 * s + 1]};
+    if (key_eq(slot, key)) return true;
+    if (key_is_empty_pattern(slot)) return false;
+    s = (s + 1) & t.mask;
+  }
+  return false;
+}
+
+struct LookupArgs {
+  TableView t;
+  const uint8_t *hashes;
+  const int64_t *blk_offsets;
+  int32_t n;
+  int64_t n_blocks;
+  int32_t *hit_blocks;
+};
+
+// G lanes per request take G consecutive blocks at a time; a ballot over the
+// group finds the first miss, and the group stops at the first chunk that
+// holds one.
+template <int G>
+__global__ __launch_bounds__(256) void k_lookup(LookupArgs a) {
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t r = gid / G;
+  if (r >= a.n) return;  // groups never straddle this test: 256 % G == 0
+  const int sub = (int)(gid % G);
+  const int lane = threadIdx.x & 63;
+  const int base = lane & ~(G - 1);
+  const uint64_t gmask = (G == 64) ? ~0ull : (((1ull << G) - 1ull) << base);
+  const int64_t b0 = a.blk_offsets[r], b1 = a.blk_offsets[r + 1];
+  if (b0 < 0 || b1 < b0 || b1 > a.n_blocks) {
+    if (sub == 0) {
+      atomicCAS(&a.t.meta->status, 0, KVGOV_E_OFFSETS);
+      a.hit_blocks[r] = 0;
+    }
+    return;
+  }
+  const bool ones = a.t.meta->ones_present != 0;
+  const int64_t nf = b1 - b0;
+  int64_t hit = nf;
+  for (int64_t j0 = 0; j0 < nf; j0 += G) {
+    const int64_t j = j0 + sub;
+    bool miss = false;
+    if (j < nf) miss = !probe(a.t, load_key(a.hashes + (b0 + j) * 32), ones);
+    const uint64_t m = __ballot(miss) & gmask;
+    if (m) {
+      hit = j0 + (__builtin_ctzll(m) - base);
+      break;
+    }
+  }
+  if (sub == 0) a.hit_blocks[r] = (int32_t)hit;
+}
+
+__global__ void k_export_begin(CacheMeta *m) { m->exported = 0; }
+
+__global__ __launch_bounds__(256) void k_export(TableView t, uint8_t *out, int64_t cap) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  const int64_t slots = (int64_t)t.mask + 1;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (gid == 0 && t.meta->ones_present) {
+    const unsigned long long at = atomicAdd(&t.meta->exported, 1ull);
+    if ((int64_t)at < cap) {
+      u32x4 *q = reinterpret_cast<u32x4 *>(out + at * 32);
+      q[0] = u32x4{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+      q[1] = q[0];
+    }
+  }
+  for (int64_t s = gid; s < slots; s += stride) {
+    if (t.tags[s] == 0) continue;
+    const unsigned long long at = atomicAdd(&t.meta->exported, 1ull);
+    if ((int64_t)at < cap) {
+      u32x4 *q = reinterpret_cast<u32x4 *>(out + at * 32);
+      q[0] = t.keys[2 * s];
+      q[1] = t.keys[2 * s + 1];
+    }
+  }
+}
+
+}  // namespace kvgov
+
+using namespace kvgov;
+
+struct kvgov_cache {
+  int device;
+  int32_t log2_slots;
+  int64_t slots;
+  TableView view;
+  std::atomic<uint32_t> epoch;
+};
+
+namespace {
+
+int check_device(const kvgov_cache *c) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return KVGOV_E_HIP;
+  return dev == c->device ? KVGOV_OK : KVGOV_E_DEVICE;
+}
+
+unsigned grid_for(int64_t work, int per_cu) {
+  const int64_t cap = (int64_t)device_cu_count() * per_cu;
+  return (unsigned)std::max<int64_t>(1, std::min<int64_t>(ceil_div(work, 256), cap));
+}
+
+int enqueue_clear(kvgov_cache *c, hipStream_t s) {
+  hipLaunchKernelGGL(k_cache_fill, dim3(grid_for(c->slots, 64)), dim3(256), 0, s, c->view.keys,
+                     c->view.tags, c->slots);
+  hipLaunchKernelGGL(k_meta_reset, dim3(1), dim3(1), 0, s, c->view.meta);
+  c->epoch.store(0);
+  return launch_status();
+}
+
+int read_meta(kvgov_cache *c, CacheMeta *m, hipStream_t s) {
+  if (hipMemcpyAsync(m, c->view.meta, sizeof(CacheMeta), hipMemcpyDeviceToHost, s) !=
+      hipSuccess)
+    return KVGOV_E_HIP;
+  if (hipStreamSynchronize(s) != hipSuccess) return KVGOV_E_HIP;
+  return KVGOV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kvgov_cache_create(int32_t log2_slots, kvgov_cache **out) {
+  if (!out || log2_slots < KVGOV_MIN_LOG2_SLOTS || log2_slots > KVGOV_MAX_LOG2_SLOTS)
+    return KVGOV_E_INVAL;
+  *out = nullptr;
+  kvgov_cache *c = new (std::nothrow) kvgov_cache();
+  if (!c) return KVGOV_E_NOMEM;
+  if (hipGetDevice(&c->device) != hipSuccess) {
+    delete c;
+    return KVGOV_E_HIP;
+  }
+  c->log2_slots = log2_slots;
+  c->slots = (int64_t)1 << log2_slots;
+  c->view.mask = (uint64_t)c->slots - 1;
+  void *keys = nullptr, *tags = nullptr, *meta = nullptr;
+  if (hipMalloc(&keys, (size_t)c->slots * 32) != hipSuccess ||
+      hipMalloc(&tags, (size_t)c->slots * 8) != hipSuccess ||
+      hipMalloc(&meta, sizeof(CacheMeta)) != hipSuccess) {
+    if (keys) (void)hipFree(keys);
+    if (tags) (void)hipFree(tags);
+    if (meta) (void)hipFree(meta);
+    delete c;
+    return KVGOV_E_NOMEM;
+  }
+  c->view.keys = static_cast<u32x4 *>(keys);
+  c->view.tags = static_cast<unsigned long long *>(tags);
+  c->view.meta = static_cast<CacheMeta *>(meta);
+  int rc = enqueue_clear(c, nullptr);
+  if (rc == KVGOV_OK && hipStreamSynchronize(nullptr) != hipSuccess) rc = KVGOV_E_HIP;
+  if (rc != KVGOV_OK) {
+    kvgov_cache_destroy(c);
+    return rc;
+  }
+  *out = c;
+  return KVGOV_OK;
+}
+
+int kvgov_cache_destroy(kvgov_cache *c) {
+  if (!c) return KVGOV_OK;
+  int rc = KVGOV_OK;
+  if (hipDeviceSynchronize() != hipSuccess) rc = KVGOV_E_HIP;
+  if (hipFree(c->view.keys) != hipSuccess) rc = KVGOV_E_HIP;
+  if (hipFree(c->view.tags) != hipSuccess) rc = KVGOV_E_HIP;
+  if (hipFree(c->view.meta) != hipSuccess) rc = KVGOV_E_HIP;
+  delete c;
+  return rc;
+}
+
+int kvgov_cache_clear(kvgov_cache *c, void *stream) {
+  if (!c) return KVGOV_E_INVAL;
+  int rc = check_device(c);
+  if (rc != KVGOV_OK) return rc;
+  return enqueue_clear(c, as_stream(stream));
+}
+
+int kvgov_cache_slots(const kvgov_cache *c, int64_t *slots) {
+  if (!c || !slots) return KVGOV_E_INVAL;
+  *slots = c->slots;
+  return KVGOV_OK;
+}
+
+int kvgov_cache_insert(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,
+                       int32_t n, int64_t n_blocks, int64_t *n_new, void *stream) {
+  if (!c || !blk_offsets || n < 0 || n_blocks < 0 || (n_blocks > 0 && !hashes))
+    return KVGOV_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(hashes) & 3) return KVGOV_E_INVAL;
+  int rc = check_device(c);
+  if (rc != KVGOV_OK) return rc;
+  hipStream_t s = as_stream(stream);
+  uint32_t epoch = c->epoch.fetch_add(1) + 1;
+  if (epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;  // 2^32 - 1 inserts since clear
+  hipLaunchKernelGGL(k_insert_begin, dim3(1), dim3(1), 0, s, c->view.meta, blk_offsets, n,
+                     n_blocks);
+  hipLaunchKernelGGL(k_insert, dim3(grid_for(n_blocks, 32)), dim3(256), 0, s, c->view, hashes,
+                     blk_offsets, n, epoch);
+  rc = launch_status();
+  if (rc != KVGOV_OK || !n_new) return rc;
+  CacheMeta m{};
+  rc = read_meta(c, &m, s);
+  if (rc != KVGOV_OK) return rc;
+  *n_new = (int64_t)m.last_new;
+  return m.status;
+}
+
+// Lanes per request for lookup: enough groups in flight to cover the chip
+// (about 2^18 lanes), one lane each when the batch alone is that large.
+static int lookup_group(int32_t n) {
+  int g = 1;
+  while (g < 64 && (int64_t)n * g * 2 <= (1 << 18)) g <<= 1;
+  return g;
+}
+
+int kvgov_cache_lookup(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,
+                       int32_t n, int64_t n_blocks, int32_t *hit_blocks, void *stream) {
+  if (!c || !blk_offsets || n < 0 || n_blocks < 0 || (n_blocks > 0 && !hashes) ||
+      (n > 0 && !hit_blocks))
+    return KVGOV_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(hashes) & 3) return KVGOV_E_INVAL;
+  int rc = check_device(c);
+  if (rc != KVGOV_OK) return rc;
+  if (n == 0) return KVGOV_OK;
+  hipStream_t s = as_stream(stream);
+  LookupArgs a{c->view, hashes, blk_offsets, n, n_blocks, hit_blocks};
+  const int g = lookup_group(n);
+  const dim3 grid((unsigned)ceil_div((int64_t)n * g, 256)), block(256);
+  switch (g) {
+    case 1: hipLaunchKernelGGL(k_lookup<1>, grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL(k_lookup<2>, grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL(k_lookup<4>, grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL(k_lookup<8>, grid, block, 0, s, a); break;
+    case 16: hipLaunchKernelGGL(k_lookup<16>, grid, block, 0, s, a); break;
+    case 32: hipLaunchKernelGGL(k_lookup<32>, grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL(k_lookup<64>, grid, block, 0, s, a); break;
+  }
+  return launch_status();
+}
+
+int kvgov_cache_count(kvgov_cache *c, int64_t *n_keys, void *stream) {
+  if (!c || !n_keys) return KVGOV_E_INVAL;
+  int rc = check_device(c);
+  if (rc != KVGOV_OK) return rc;
+  CacheMeta m{};
+  rc = read_meta(c, &m, as_stream(stream));
+  if (rc != KVGOV_OK) return rc;
+  *n_keys = (int64_t)m.n_keys;
+  return m.status;
+}
+
+int kvgov_cache_export(kvgov_cache *c, uint8_t *keys, int64_t cap, int64_t *n_keys,
+                       void *stream) {
+  if (!c || !n_keys || cap < 0 || (cap > 0 && !keys)) return KVGOV_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(keys) & 3) return KVGOV_E_INVAL;
+  int rc = check_device(c);
+  if (rc != KVGOV_OK) return rc;
+  hipStream_t s = as_stream(stream);
+  hipLaunchKernelGGL(k_export_begin, dim3(1), dim3(1), 0, s, c->view.meta);
+  hipLaunchKernelGGL(k_export, dim3(grid_for(c->slots, 32)), dim3(256), 0, s, c->view, keys,
+                     cap);
+  rc = launch_status();
+  if (rc != KVGOV_OK) return rc;
+  CacheMeta m{};
+  rc = read_meta(c, &m, s);
+  if (rc != KVGOV_OK) return rc;
+  *n_keys = (int64_t)m.exported;
+  return (int64_t)m.exported > cap ? KVGOV_E_CAPACITY : KVGOV_OK;
+}
+
+}  // extern "C"

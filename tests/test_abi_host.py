@@ -1,0 +1,111 @@
+"""The C ABI without a GPU: the library loads, exports every declared call,
+and rejects bad arguments on the host before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_09225_amd import kvgov as K
+
+HEADER = K.HEADER_PATH
+pytestmark = pytest.mark.skipif(not os.path.exists(K.LIB_PATH),
+                                reason="libkvgov.so not built")
+
+
+def _declared():
+    with open(HEADER) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvgov_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared()
+    assert len(names) >= 13, names
+    L = ctypes.CDLL(K.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+    # and the binding covers exactly the declared calls
+    assert sorted(K._SIGNATURES) == names
+
+
+def test_header_constants_match_binding():
+    c = K.header_constants()
+    assert (c["KVGOV_NONE"], c["KVGOV_ROOT"], c["KVGOV_BOUNDARY"]) == (K.NONE, K.ROOT, K.BOUNDARY)
+    assert c["KVGOV_BLOCK_SIZE"] == K.BLOCK == 16
+    assert c["KVGOV_OK"] == 0
+    codes = [v for k, v in c.items() if k.startswith("KVGOV_E_")]
+    assert len(codes) == len(set(codes)) and all(v < 0 for v in codes)
+    L = K.lib()
+    for name, v in c.items():
+        if name.startswith("KVGOV_E_"):
+            assert K.strerror(v) != "unknown error code", name
+    assert K.strerror(12345) == "unknown error code"
+    assert L.kvgov_version() >> 16 == 1
+
+
+def test_host_validation_returns_before_any_launch():
+    c = K.header_constants()
+    INVAL, UNSUP = c["KVGOV_E_INVAL"], c["KVGOV_E_UNSUPPORTED"]
+    L = K.lib()
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    key = (ctypes.c_uint8 * 65)()
+    kp = ctypes.cast(key, ctypes.c_void_p)
+    # salts
+    assert L.kvgov_salts(None, 32, fake, 32, 4, fake, None) == INVAL
+    assert L.kvgov_salts(kp, 0, fake, 32, 4, fake, None) == INVAL
+    assert L.kvgov_salts(kp, 65, fake, 32, 4, fake, None) == UNSUP
+    assert L.kvgov_salts(kp, 32, fake, -1, 4, fake, None) == INVAL
+    assert L.kvgov_salts(kp, 32, fake, 1025, 4, fake, None) == INVAL
+    assert L.kvgov_salts(kp, 32, fake, 32, -1, fake, None) == INVAL
+    assert L.kvgov_salts(kp, 32, fake, 32, 4, None, None) == INVAL
+    assert L.kvgov_salts(kp, 32, None, 0, 0, None, None) == 0  # P == 0: nothing to do
+    # block offsets
+    assert L.kvgov_block_offsets(None, 4, 16, fake, fake, None) == INVAL
+    assert L.kvgov_block_offsets(fake, -1, 16, fake, fake, None) == INVAL
+    assert L.kvgov_block_offsets(fake, 4, 8, fake, fake, None) == UNSUP
+    assert L.kvgov_block_offsets(fake, 4, 16, fake, None, None) == INVAL
+
+    def chains(**kw):
+        a = dict(tokens=fake, n_tokens=64, tok_offsets=fake, n=2, principal=fake, salts=fake,
+                 P=4, mode=K.ROOT, boundary_tok=fake, block_size=16, blk_offsets=fake,
+                 hashes=fake, n_blocks=4, status=fake, stream=None)
+        a.update(kw)
+        return L.kvgov_hash_chains(*a.values())
+
+    assert chains(n=-1) == INVAL
+    assert chains(mode=3) == INVAL
+    assert chains(block_size=32) == UNSUP
+    assert chains(status=None) == INVAL
+    assert chains(tok_offsets=None) == INVAL
+    assert chains(blk_offsets=None) == INVAL
+    assert chains(principal=None) == INVAL
+    assert chains(salts=None) == INVAL
+    assert chains(P=0) == INVAL
+    assert chains(mode=K.BOUNDARY, boundary_tok=None) == INVAL
+    assert chains(tokens=ctypes.c_void_p(0x1002)) == INVAL  # misaligned
+    assert chains(hashes=ctypes.c_void_p(0x1001)) == INVAL
+    assert chains(n=0) == 0
+    # cache
+    h = ctypes.c_void_p()
+    assert L.kvgov_cache_create(3, ctypes.byref(h)) == INVAL
+    assert L.kvgov_cache_create(32, ctypes.byref(h)) == INVAL
+    assert L.kvgov_cache_create(10, None) == INVAL
+    n = ctypes.c_int64()
+    assert L.kvgov_cache_insert(None, fake, fake, 1, 4, None, None) == INVAL
+    assert L.kvgov_cache_lookup(None, fake, fake, 1, 4, fake, None) == INVAL
+    assert L.kvgov_cache_clear(None, None) == INVAL
+    assert L.kvgov_cache_count(None, ctypes.byref(n), None) == INVAL
+    assert L.kvgov_cache_export(None, fake, 1, ctypes.byref(n), None) == INVAL
+    assert L.kvgov_cache_slots(None, ctypes.byref(n)) == INVAL
+    assert L.kvgov_cache_destroy(None) == 0
+
+
+def test_binding_fails_loudly_without_gpu():
+    """No silent CPU path: without a GPU the binding refuses CPU tensors."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    with pytest.raises((ValueError, RuntimeError)):
+        K.salts(b"k" * 32, torch.zeros((2, 32), dtype=torch.uint8))

@@ -1,0 +1,356 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Every comparison is bit-exact (digests, hit counts, key sets, n_new): the
+path computes integers only.  Slot placement inside the table is not part of
+the contract and is never compared; the exported key *set* is.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from workloads import Batch, VOCAB
+
+pytestmark = pytest.mark.gpu
+
+K = pytest.importorskip("paper_2608_09225_amd.kvgov")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    K.lib()
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def ragged(seed, lens, P=4, bt_mode="random"):
+    g = np.random.default_rng(seed)
+    lens = np.asarray(lens, dtype=np.int64)
+    offs = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    toks = g.integers(-2 ** 31, 2 ** 31 - 1, int(offs[-1]), dtype=np.int64).astype(np.int32) \
+        if bt_mode == "wide" else g.integers(0, VOCAB, int(offs[-1]), dtype=np.int32)
+    prin = g.integers(0, P, lens.size).astype(np.int32)
+    bt = np.floor(g.random(lens.size) * (lens + 1)).astype(np.int32)
+    return Batch(toks, offs, prin, bt)
+
+
+def secret(seed, P, klen=32, idlen=32):
+    g = np.random.default_rng(1000 + seed)
+    Kb = g.integers(0, 256, klen, dtype=np.uint8).tobytes()
+    ids = g.integers(0, 256, (P, idlen), dtype=np.uint8)
+    return Kb, ids
+
+
+def gpu_chains(b: Batch, salts_dev, mode, status=None, check=True):
+    return K.hash_chains(dev(b.tokens), dev(b.tok_offsets), dev(b.principal), salts_dev, mode,
+                         dev(b.boundary_tok), status=status, check=check)
+
+
+# ---------------------------------------------------------------------------
+# a1 salts
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("klen", [1, 31, 32, 55, 64])
+@pytest.mark.parametrize("idlen", [0, 1, 32, 55, 56, 64, 119, 120, 300])
+def test_salts(klen, idlen):
+    for P in (1, 65):
+        Kb, ids = secret(klen * 7 + idlen, P, klen, idlen)
+        got = K.salts(Kb, dev(ids)).cpu().numpy()
+        want = O.salts(Kb, ids)
+        for p in range(P):
+            assert bytes(got[p]) == want[p], (klen, idlen, P, p)
+
+
+def test_salts_many_principals():
+    Kb, ids = secret(3, 4096)
+    got = K.salts(Kb, dev(ids)).cpu().numpy()
+    want = O.salts(Kb, ids)
+    assert all(bytes(got[p]) == want[p] for p in range(4096))
+
+
+# ---------------------------------------------------------------------------
+# output layout
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("n", [0, 1, 1023, 1024, 1025, 5000, 70000])
+def test_block_offsets(n):
+    g = np.random.default_rng(n)
+    lens = g.integers(0, 100, n).astype(np.int64)
+    if n:
+        lens[:min(n, 8)] = [0, 15, 16, 17, 31, 32, 33, 99][:min(n, 8)]
+    b = Batch(np.zeros(int(lens.sum()), np.int32), np.concatenate([[0], np.cumsum(lens)]),
+              np.zeros(n, np.int32), np.zeros(n, np.int32))
+    got = K.block_offsets(dev(b.tok_offsets)).cpu().numpy()
+    assert np.array_equal(got, b.blk_offsets())
+
+
+def test_block_offsets_negative_length_latched():
+    offs = np.array([0, 40, 30, 50], dtype=np.int64)
+    with pytest.raises(K.KvgovError) as e:
+        K.block_offsets(dev(offs))
+    assert e.value.code == K.header_constants()["KVGOV_E_OFFSETS"]
+
+
+# ---------------------------------------------------------------------------
+# a2/a3 chains
+# ---------------------------------------------------------------------------
+
+EDGE_LENS = [0, 1, 15, 16, 17, 31, 32, 33, 47, 48, 63, 64, 65, 160, 161, 500, 1023, 1024]
+
+
+@pytest.mark.parametrize("mode", [W.NONE, W.ROOT, W.BOUNDARY])
+def test_chains_edge_lengths(mode):
+    """Ragged lengths around block edges; boundary at 0, inside, on a block
+    edge, at and past the last full block."""
+    lens = EDGE_LENS * 6
+    b = ragged(11 + mode, lens)
+    L = b.lengths
+    bt = b.boundary_tok
+    for i in range(len(lens)):
+        kind = i // len(EDGE_LENS)
+        bt[i] = [0, min(15, L[i]), min(16, L[i]), L[i] // 2, L[i], (L[i] // 16) * 16][kind]
+    Kb, ids = secret(5, 4)
+    sd = K.salts(Kb, dev(ids))
+    got = gpu_chains(b, sd, mode).cpu().numpy()
+    want = O.hash_chains(b.tokens, b.tok_offsets, b.principal, O.salts(Kb, ids), mode, bt)
+    assert got.shape == want.shape
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("mode", [W.NONE, W.ROOT, W.BOUNDARY])
+def test_chains_full_int32_range(mode):
+    b = ragged(21, [16, 48, 100, 33], bt_mode="wide")
+    Kb, ids = secret(6, 4)
+    got = gpu_chains(b, K.salts(Kb, dev(ids)), mode).cpu().numpy()
+    want = O.hash_chains(b.tokens, b.tok_offsets, b.principal, O.salts(Kb, ids), mode,
+                         b.boundary_tok)
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("mode", [W.NONE, W.ROOT, W.BOUNDARY])
+def test_chains_many_waves_and_ordering(mode):
+    """9000 requests (above the longest-first ordering threshold), lengths
+    0..400 tokens, so waves mix lengths and boundaries."""
+    g = np.random.default_rng(31)
+    lens = g.integers(0, 400, 9000)
+    b = ragged(33 + mode, lens, P=37)
+    Kb, ids = secret(7, 37)
+    got = gpu_chains(b, K.salts(Kb, dev(ids)), mode).cpu().numpy()
+    want = O.hash_chains_parallel(b.tokens, b.tok_offsets, b.principal, O.salts(Kb, ids), mode,
+                                  b.boundary_tok)
+    assert np.array_equal(got, want)
+
+
+def test_chains_unaligned_token_offsets():
+    """Requests starting at any token offset (tokens not 16-byte aligned)."""
+    b = ragged(41, [1, 35, 2, 70, 3, 17, 5, 64])
+    Kb, ids = secret(8, 4)
+    sd = K.salts(Kb, dev(ids))
+    for mode in (W.NONE, W.ROOT, W.BOUNDARY):
+        got = gpu_chains(b, sd, mode).cpu().numpy()
+        want = O.hash_chains(b.tokens, b.tok_offsets, b.principal, O.salts(Kb, ids), mode,
+                             b.boundary_tok)
+        assert np.array_equal(got, want)
+
+
+def test_chains_rejects_bad_requests_and_keeps_the_rest():
+    c = K.header_constants()
+    b = ragged(51, [64, 64, 64, 64, 64])
+    Kb, ids = secret(9, 4)
+    sd = K.salts(Kb, dev(ids))
+    want = O.hash_chains(b.tokens, b.tok_offsets, b.principal, O.salts(Kb, ids), W.BOUNDARY,
+                         b.boundary_tok)
+    for field, val, code in (("principal", 4, "KVGOV_E_PRINCIPAL"),
+                             ("principal", -1, "KVGOV_E_PRINCIPAL"),
+                             ("boundary_tok", 65, "KVGOV_E_BOUNDARY"),
+                             ("boundary_tok", -1, "KVGOV_E_BOUNDARY")):
+        bb = Batch(b.tokens, b.tok_offsets, b.principal.copy(), b.boundary_tok.copy())
+        getattr(bb, field)[2] = val
+        status = K.new_status()
+        out = torch.full((20, 32), 7, dtype=torch.uint8, device="cuda")
+        K.hash_chains(dev(bb.tokens), dev(bb.tok_offsets), dev(bb.principal), sd, W.BOUNDARY,
+                      dev(bb.boundary_tok), blk_offsets=dev(b.blk_offsets()), out=out,
+                      status=status, check=False)
+        assert int(status.item()) == c[code], (field, val)
+        o = out.cpu().numpy()
+        assert np.array_equal(o[:8], want[:8]) and np.array_equal(o[12:], want[12:])
+        assert np.all(o[8:12] == 7)  # the rejected request wrote nothing
+    # blk_offsets that do not match len // 16, and a hashes buffer too small
+    status = K.new_status()
+    bo = b.blk_offsets().copy()
+    bo[3] += 1
+    out = torch.zeros((21, 32), dtype=torch.uint8, device="cuda")
+    K.hash_chains(dev(b.tokens), dev(b.tok_offsets), dev(b.principal), sd, W.ROOT,
+                  blk_offsets=dev(bo), out=out, status=status, check=False)
+    assert int(status.item()) == c["KVGOV_E_OFFSETS"]
+    status = K.new_status()
+    out = torch.zeros((19, 32), dtype=torch.uint8, device="cuda")
+    K.hash_chains(dev(b.tokens), dev(b.tok_offsets), dev(b.principal), sd, W.ROOT,
+                  blk_offsets=dev(b.blk_offsets()), out=out, status=status, check=False)
+    assert int(status.item()) == c["KVGOV_E_OFFSETS"]
+
+
+def test_chains_invariants_on_gpu():
+    """Root salting equals boundary salting at k = 0; boundary past the last
+    block equals no salting; blocks below k are shared across principals."""
+    b = ragged(61, [300] * 64)
+    Kb, ids = secret(10, 4)
+    sd = K.salts(Kb, dev(ids))
+    none = gpu_chains(b, sd, W.NONE).cpu().numpy()
+    root = gpu_chains(b, sd, W.ROOT).cpu().numpy()
+    b0 = Batch(b.tokens, b.tok_offsets, b.principal, np.zeros(64, np.int32))
+    assert np.array_equal(gpu_chains(b0, sd, W.BOUNDARY).cpu().numpy(), root)
+    bL = Batch(b.tokens, b.tok_offsets, b.principal, np.full(64, 300, np.int32))
+    assert np.array_equal(gpu_chains(bL, sd, W.BOUNDARY).cpu().numpy(), none)
+    bk = Batch(b.tokens, b.tok_offsets, b.principal, np.full(64, 100, np.int32))
+    bnd = gpu_chains(bk, sd, W.BOUNDARY).cpu().numpy().reshape(64, 18, 32)
+    assert np.array_equal(bnd[:, :6], none.reshape(64, 18, 32)[:, :6])
+
+
+# ---------------------------------------------------------------------------
+# a4/a5 cache
+# ---------------------------------------------------------------------------
+
+def key_set(arr):
+    raw = np.ascontiguousarray(arr).tobytes()
+    return {raw[i:i + 32] for i in range(0, len(raw), 32)}
+
+
+def test_cache_insert_lookup_small():
+    b = ragged(71, W_LENS := [0, 15, 16, 17, 100, 256, 300, 32] * 8, P=3)
+    Kb, ids = secret(11, 3)
+    sd = K.salts(Kb, dev(ids))
+    hs = gpu_chains(b, sd, W.ROOT)
+    bo = dev(b.blk_offsets())
+    want_h = O.hash_chains(b.tokens, b.tok_offsets, b.principal, O.salts(Kb, ids), W.ROOT)
+    with K.Cache(10) as c:
+        assert c.slots() == 1024
+        assert c.lookup(hs, bo).cpu().numpy().tolist() == [0] * len(W_LENS)
+        half = dev(b.blk_offsets()[:33])
+        T = O.Table()
+        assert c.insert(hs, half) == T.insert(want_h, b.blk_offsets()[:33])
+        assert np.array_equal(c.lookup(hs, bo).cpu().numpy(), T.lookup(want_h, b.blk_offsets()))
+        assert c.insert(hs, half) == 0
+        assert c.insert(hs, bo) == T.insert(want_h, b.blk_offsets())
+        got = c.lookup(hs, bo).cpu().numpy()
+        assert np.array_equal(got, T.lookup(want_h, b.blk_offsets()))
+        assert np.array_equal(got, b.lengths // 16)
+        assert c.count() == len(T.keys)
+        assert key_set(c.export().cpu().numpy()) == T.keys
+
+
+def test_cache_duplicates_and_special_keys():
+    """Duplicate keys in one batch count once; the all-zero and all-0xFF keys
+    (the latter is the empty-slot pattern) are ordinary keys."""
+    g = np.random.default_rng(81)
+    base = g.integers(0, 256, (300, 32), dtype=np.uint8)
+    base[0] = 0
+    base[1] = 255
+    base[2, :31] = 255  # one byte away from the empty pattern
+    keys = np.concatenate([base, base[::-1], base[:50]])
+    g.shuffle(keys)
+    bo = np.array([0, keys.shape[0]], dtype=np.int64)
+    with K.Cache(12) as c:
+        assert c.insert(dev(keys), dev(bo)) == 300
+        assert c.insert(dev(keys), dev(bo)) == 0
+        assert c.count() == 300
+        assert key_set(c.export().cpu().numpy()) == key_set(base)
+        # each special key alone as a one-block request
+        q = np.stack([base[0], base[1], base[2], g.integers(0, 256, 32, dtype=np.uint8)])
+        hits = c.lookup(dev(q), dev(np.arange(5, dtype=np.int64))).cpu().numpy()
+        assert hits.tolist() == [1, 1, 1, 0]
+    with K.Cache(6) as c:  # 64 slots
+        q = np.stack([np.full(32, 255, np.uint8)])
+        assert c.lookup(dev(q), dev(np.array([0, 1], np.int64))).cpu().numpy().tolist() == [0]
+        assert c.insert(dev(q), dev(np.array([0, 1], np.int64))) == 1
+        assert c.lookup(dev(q), dev(np.array([0, 1], np.int64))).cpu().numpy().tolist() == [1]
+
+
+def test_cache_heavy_duplicates_repeatable():
+    """Many lanes insert the same few keys at once; results and key sets are
+    identical run after run."""
+    g = np.random.default_rng(91)
+    uniq = g.integers(0, 256, (37, 32), dtype=np.uint8)
+    keys = uniq[g.integers(0, 37, 200000)]
+    bo = np.array([0, keys.shape[0]], dtype=np.int64)
+    for _ in range(3):
+        with K.Cache(8) as c:
+            assert c.insert(dev(keys), dev(bo)) == 37
+            assert key_set(c.export().cpu().numpy()) == key_set(uniq)
+
+
+def test_cache_full_is_latched():
+    c_ = K.header_constants()
+    g = np.random.default_rng(101)
+    keys = g.integers(0, 256, (40, 32), dtype=np.uint8)
+    with K.Cache(4) as c:  # 16 slots
+        with pytest.raises(K.KvgovError) as e:
+            c.insert(dev(keys), dev(np.array([0, 40], np.int64)))
+        assert e.value.code == c_["KVGOV_E_FULL"]
+        got = key_set(c.export(cap=64).cpu().numpy()) if c.slots() else set()
+        assert len(got) == 16 and got <= key_set(keys)
+        c.clear()
+        assert c.count() == 0
+        assert c.insert(dev(keys[:10]), dev(np.array([0, 10], np.int64))) == 10
+
+
+def test_cache_bad_offsets_latched():
+    c_ = K.header_constants()
+    keys = np.zeros((4, 32), np.uint8)
+    with K.Cache(6) as c:
+        with pytest.raises(K.KvgovError) as e:
+            c.insert(dev(keys), dev(np.array([0, 5], np.int64)))
+        assert e.value.code == c_["KVGOV_E_OFFSETS"]
+        c.clear()
+        hits = c.lookup(dev(keys), dev(np.array([0, 2, 1, 9], np.int64)))
+        assert hits.cpu().numpy().tolist()[1:] == [0, 0]
+        with pytest.raises(K.KvgovError):
+            c.count()
+
+
+@pytest.mark.parametrize("n_req", [1, 7, 64, 5000, 300000])
+def test_cache_lookup_group_sizes(n_req):
+    """Lookups at batch sizes that select every lanes-per-request width."""
+    g = np.random.default_rng(n_req)
+    nb = g.integers(0, 70, n_req).astype(np.int64)
+    bo = np.concatenate([[0], np.cumsum(nb)])
+    keys = g.integers(0, 256, (int(bo[-1]), 32), dtype=np.uint8)
+    # insert a random prefix of each request's keys
+    pre = np.floor(g.random(n_req) * (nb + 1)).astype(np.int64)
+    ins = np.concatenate([keys[bo[r]:bo[r] + pre[r]] for r in range(n_req)] +
+                         [np.zeros((0, 32), np.uint8)])
+    with K.Cache(max(6, int(np.ceil(np.log2(max(ins.shape[0], 1) * 2 + 1))))) as c:
+        if ins.shape[0]:
+            c.insert(dev(ins), dev(np.array([0, ins.shape[0]], np.int64)))
+        hits = c.lookup(dev(keys), dev(bo)).cpu().numpy()
+    assert np.array_equal(hits, pre)
+
+
+# ---------------------------------------------------------------------------
+# the small workload end to end
+# ---------------------------------------------------------------------------
+
+def test_tiny_workload_end_to_end():
+    wl = W.make("tiny")
+    sd = K.salts(wl.K, dev(wl.principal_ids))
+    want_s = O.salts(wl.K, wl.principal_ids)
+    hi = gpu_chains(wl.insert, sd, W.ROOT)
+    hl = gpu_chains(wl.lookup, sd, W.ROOT)
+    T = O.Table()
+    wi = O.hash_chains(wl.insert.tokens, wl.insert.tok_offsets, wl.insert.principal, want_s, W.ROOT)
+    wlk = O.hash_chains(wl.lookup.tokens, wl.lookup.tok_offsets, wl.lookup.principal, want_s,
+                        W.ROOT)
+    assert np.array_equal(hi.cpu().numpy(), wi) and np.array_equal(hl.cpu().numpy(), wlk)
+    with K.Cache(wl.log2_slots) as c:
+        assert c.insert(hi, dev(wl.insert.blk_offsets())) == T.insert(wi)
+        hits = c.lookup(hl, dev(wl.lookup.blk_offsets())).cpu().numpy()
+    assert np.array_equal(hits, T.lookup(wlk, wl.lookup.blk_offsets()))
+    assert np.array_equal(hits, wl.lookup.expect_hits[W.ROOT])
