@@ -42,13 +42,11 @@ namespace kvgov {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4), aligned(4)));
 
 struct CacheMeta {
-  unsigned long long n_keys;      // keys in the table (all-0xFF key included)
-  unsigned long long last_new;    // keys added by the latest insert
-  unsigned long long exported;    // keys written by the latest export
-  int32_t status;                 // latched error (0 = none)
-  int32_t ones_present;           // the all-0xFF key is in the table
-  int32_t call_bad;               // the current call was rejected by a kernel
-  int32_t pad_;
+  unsigned long long n_keys;       // keys in the table (all-0xFF key included)
+  unsigned long long new_keys[2];  // keys added by insert call `epoch`, at [epoch & 1]
+  unsigned long long exported;     // keys written by the latest export
+  int32_t status;                  // latched error (0 = none)
+  int32_t ones_present;            // the all-0xFF key is in the table
 };
 
 struct TableView {
@@ -97,33 +95,22 @@ __device__ __forceinline__ uint64_t slot_hash(const Key &k) {
 // ---------------------------------------------------------------------------
 
 __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long long *tags,
-                                                    int64_t slots) {
+                                                    int64_t slots, CacheMeta *m) {
   const int64_t stride = (int64_t)gridDim.x * 256;
   const u32x4 ones = u32x4{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    m->n_keys = 0;
+    m->new_keys[0] = 0;
+    m->new_keys[1] = 0;
+    m->exported = 0;
+    m->status = 0;
+    m->ones_present = 0;
+  }
   for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < slots; s += stride) {
     keys[2 * s] = ones;
     keys[2 * s + 1] = ones;
     tags[s] = 0;
   }
-}
-
-__global__ void k_meta_reset(CacheMeta *m) {
-  m->n_keys = 0;
-  m->last_new = 0;
-  m->exported = 0;
-  m->status = 0;
-  m->ones_present = 0;
-  m->call_bad = 0;
-}
-
-// Start of an insert: zero the per-call counter and check the key range.
-__global__ void k_insert_begin(CacheMeta *m, const int64_t *blk_offsets, int32_t n,
-                               int64_t n_blocks) {
-  m->last_new = 0;
-  const int64_t lo = blk_offsets[0], hi = blk_offsets[n];
-  const bool bad = lo < 0 || hi < lo || hi > n_blocks || hi - lo >= 0xFFFFFFFFll;
-  m->call_bad = bad ? 1 : 0;
-  if (bad) atomicCAS(&m->status, 0, KVGOV_E_OFFSETS);
 }
 
 __device__ __forceinline__ void add_wave_count(unsigned long long *dst1,
@@ -140,11 +127,19 @@ __device__ __forceinline__ void add_wave_count(unsigned long long *dst1,
   }
 }
 
+// Tags only ever change from 0 to a claim, so a plain (possibly stale) read
+// can only show 0 for a claimed slot; the compare-and-swap that follows then
+// fails and returns the claim.  Coherent atomics are used for the claim only.
 __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hashes,
                                                 const int64_t *blk_offsets, int32_t n,
-                                                uint32_t epoch) {
-  if (__hip_atomic_load(&t.meta->call_bad, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+                                                int64_t n_blocks, uint32_t epoch) {
   const int64_t lo = blk_offsets[0], hi = blk_offsets[n];
+  const bool first = blockIdx.x == 0 && threadIdx.x == 0;
+  if (first) t.meta->new_keys[(epoch + 1) & 1] = 0;  // counter of the next call
+  if (lo < 0 || hi < lo || hi > n_blocks || hi - lo >= 0xFFFFFFFFll) {
+    if (first) atomicCAS(&t.meta->status, 0, KVGOV_E_OFFSETS);
+    return;
+  }
   const int64_t stride = (int64_t)gridDim.x * 256;
   const uint64_t slots = t.mask + 1;
   uint32_t added = 0;
@@ -159,8 +154,7 @@ __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hash
     uint64_t s = slot_hash(key) & t.mask;
     uint64_t probes = 0;
     while (true) {
-      unsigned long long tag =
-          __hip_atomic_load(&t.tags[s], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      unsigned long long tag = t.tags[s];
       if (tag == 0) {
         unsigned long long expect = 0;
         if (__hip_atomic_compare_exchange_strong(&t.tags[s], &expect, mine, __ATOMIC_RELAXED,
@@ -188,7 +182,7 @@ __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hash
       }
     }
   }
-  add_wave_count(&t.meta->last_new, &t.meta->n_keys, added);
+  add_wave_count(&t.meta->new_keys[epoch & 1], &t.meta->n_keys, added);
 }
 
 // Is `key` in the table?  Reads the key array only.
@@ -301,8 +295,7 @@ unsigned grid_for(int64_t work, int per_cu) {
 
 int enqueue_clear(kvgov_cache *c, hipStream_t s) {
   hipLaunchKernelGGL(k_cache_fill, dim3(grid_for(c->slots, 64)), dim3(256), 0, s, c->view.keys,
-                     c->view.tags, c->slots);
-  hipLaunchKernelGGL(k_meta_reset, dim3(1), dim3(1), 0, s, c->view.meta);
+                     c->view.tags, c->slots, c->view.meta);
   c->epoch.store(0);
   return launch_status();
 }
@@ -389,16 +382,14 @@ int kvgov_cache_insert(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
   hipStream_t s = as_stream(stream);
   uint32_t epoch = c->epoch.fetch_add(1) + 1;
   if (epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;  // 2^32 - 1 inserts since clear
-  hipLaunchKernelGGL(k_insert_begin, dim3(1), dim3(1), 0, s, c->view.meta, blk_offsets, n,
-                     n_blocks);
   hipLaunchKernelGGL(k_insert, dim3(grid_for(n_blocks, 32)), dim3(256), 0, s, c->view, hashes,
-                     blk_offsets, n, epoch);
+                     blk_offsets, n, n_blocks, epoch);
   rc = launch_status();
   if (rc != KVGOV_OK || !n_new) return rc;
   CacheMeta m{};
   rc = read_meta(c, &m, s);
   if (rc != KVGOV_OK) return rc;
-  *n_new = (int64_t)m.last_new;
+  *n_new = (int64_t)m.new_keys[epoch & 1];
   return m.status;
 }
 

@@ -121,7 +121,7 @@ __global__ __launch_bounds__(64) void k_salts(SaltArgs a) {
   set_iv(st);
 #pragma unroll
   for (int i = 0; i < 16; ++i) w[i] = a.key[i] ^ 0x36363636u;
-  compress_rolled(st, w);
+  compress(st, w);
   const int nblk = (L + 9 + 63) / 64;  // id, 0x80, 64-bit length
   for (int blk = 0; blk < nblk; ++blk) {
 #pragma unroll
@@ -140,20 +140,20 @@ __global__ __launch_bounds__(64) void k_salts(SaltArgs a) {
       w[14] = (uint32_t)(bits >> 32);
       w[15] = (uint32_t)bits;
     }
-    compress_rolled(st, w);
+    compress(st, w);
   }
   uint32_t o[8];
   set_iv(o);
 #pragma unroll
   for (int i = 0; i < 16; ++i) w[i] = a.key[i] ^ 0x5c5c5c5cu;
-  compress_rolled(o, w);
+  compress(o, w);
 #pragma unroll
   for (int i = 0; i < 8; ++i) w[i] = st[i];
   w[8] = 0x80000000u;
 #pragma unroll
   for (int i = 9; i < 15; ++i) w[i] = 0;
   w[15] = (64 + 32) * 8;
-  compress_rolled(o, w);
+  compress(o, w);
   store_digest(a.salts + (int64_t)p * 32, o);
 }
 
@@ -210,18 +210,16 @@ __global__ __launch_bounds__(kScanThreads) void k_blk_partial(const int64_t *tok
 __global__ __launch_bounds__(kScanThreads) void k_blk_scan_partials(int64_t *partial,
                                                                     int64_t count) {
   __shared__ int64_t lds[kScanThreads / 64];
+  __shared__ int64_t chunk_total;
   int64_t carry = 0;
   for (int64_t base = 0; base < count; base += kScanThreads) {
     const int64_t i = base + threadIdx.x;
     const int64_t v = i < count ? partial[i] : 0;
     const int64_t inc = block_inclusive_scan(v, lds);
     if (i < count) partial[i] = carry + inc - v;
-    const int64_t total = __shfl(inc, 63, 64);  // per-wave value, fixed below
-    (void)total;
-    __shared__ int64_t last;
-    if (threadIdx.x == kScanThreads - 1) last = inc;
+    if (threadIdx.x == kScanThreads - 1) chunk_total = inc;
     __syncthreads();
-    carry += last;
+    carry += chunk_total;
     __syncthreads();
   }
 }
@@ -326,8 +324,8 @@ struct ChainArgs {
 };
 
 template <int MODE>
-__global__ __launch_bounds__(64) void k_chains(ChainArgs a) {
-  const int32_t i = blockIdx.x * kWave + threadIdx.x;
+__global__ __launch_bounds__(256) void k_chains(ChainArgs a) {
+  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.n) return;
   const int32_t r = a.order ? a.order[i] : i;
 
@@ -438,6 +436,27 @@ __global__ __launch_bounds__(64) void k_chains(ChainArgs a) {
 // host side
 // ---------------------------------------------------------------------------
 
+// Dynamic LDS per chain workgroup: just over half a CU's LDS.
+static size_t chain_lds_reserve() {
+  static std::mutex mu;
+  static std::vector<size_t> per_dev;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 96 * 1024;
+  std::lock_guard<std::mutex> g(mu);
+  if ((int)per_dev.size() <= dev) per_dev.resize(dev + 1, 0);
+  if (per_dev[dev] == 0) {
+    int cu_lds = 0, blk_lds = 0;
+    if (hipDeviceGetAttribute(&cu_lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+            hipSuccess || cu_lds <= 0)
+      cu_lds = 160 * 1024;
+    if (hipDeviceGetAttribute(&blk_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
+            hipSuccess || blk_lds <= 0)
+      blk_lds = cu_lds;
+    per_dev[dev] = std::min<size_t>((size_t)cu_lds / 2 + 4096, (size_t)blk_lds);
+  }
+  return per_dev[dev];
+}
+
 int device_cu_count() {
   static std::mutex mu;
   static std::vector<int> cus;
@@ -523,9 +542,10 @@ int kvgov_block_offsets(const int64_t *tok_offsets, int32_t n, int32_t block_siz
   return rc;
 }
 
-// Batches smaller than this run in input order: they fill at most a few
-// waves per SIMD, so ordering cannot shorten the longest chain.
-static constexpr int32_t kOrderMinRequests = 8192;
+// Longest-first ordering pays once the batch has about as many waves as the
+// chip has SIMDs; below that every wave has a SIMD of its own from the start
+// and the kernel takes as long as its longest chain in any order.
+static int64_t order_min_requests() { return (int64_t)device_cu_count() * 4 * kWave / 2; }
 
 int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_offsets,
                       int32_t n, const int32_t *principal, const uint8_t *salts, int32_t P,
@@ -560,7 +580,7 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
   a.order = nullptr;
 
   int32_t *scratch = nullptr;
-  if (n >= kOrderMinRequests) {
+  if (n >= order_min_requests()) {
     const size_t bytes = sizeof(int32_t) * ((size_t)kOrderBuckets + (size_t)n);
     if (hipMallocAsync(reinterpret_cast<void **>(&scratch), bytes, s) != hipSuccess)
       return KVGOV_E_NOMEM;
@@ -575,11 +595,21 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
                        tok_offsets, n, hist, order);
     a.order = order;
   }
-  const dim3 grid((unsigned)ceil_div(n, kWave)), block(kWave);
+  // Launch shape.  A chain wave is bound by its SIMD's issue rate, so it
+  // should never share a SIMD while others sit idle.  The dispatcher stacks
+  // the waves of concurrent launches on the same SIMDs, and the older wave
+  // then takes nearly every issue slot, so the workgroup reserves more than
+  // half of a CU's LDS (unused by the kernel): at most one chain workgroup
+  // per CU.  Batches of at most one wave per CU run one wave per workgroup
+  // (one SIMD per CU busy, every CU used); larger ones run four waves per
+  // workgroup, one per SIMD.
+  const int threads = (int64_t)n <= (int64_t)device_cu_count() * kWave ? kWave : 4 * kWave;
+  const dim3 grid((unsigned)ceil_div(n, threads)), block(threads);
+  const size_t lds = chain_lds_reserve();
   switch (mode) {
-    case KVGOV_NONE: hipLaunchKernelGGL(k_chains<KVGOV_NONE>, grid, block, 0, s, a); break;
-    case KVGOV_ROOT: hipLaunchKernelGGL(k_chains<KVGOV_ROOT>, grid, block, 0, s, a); break;
-    default: hipLaunchKernelGGL(k_chains<KVGOV_BOUNDARY>, grid, block, 0, s, a); break;
+    case KVGOV_NONE: hipLaunchKernelGGL(k_chains<KVGOV_NONE>, grid, block, lds, s, a); break;
+    case KVGOV_ROOT: hipLaunchKernelGGL(k_chains<KVGOV_ROOT>, grid, block, lds, s, a); break;
+    default: hipLaunchKernelGGL(k_chains<KVGOV_BOUNDARY>, grid, block, lds, s, a); break;
   }
   int rc = launch_status();
   if (scratch && hipFreeAsync(scratch, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;

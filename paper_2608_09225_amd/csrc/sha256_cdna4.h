@@ -9,7 +9,7 @@
 //   rotate right      v_alignbit_b32 x, x, n
 //   three-way xor     v_bitop3_b32 (truth table 0x96)
 //   majority          v_bitop3_b32 (truth table 0xE8)
-//   choose            v_bfi_b32 / v_bitop3_b32
+//   choose            v_bitop3_b32 (truth table 0xCA)
 //   three-input add   v_add3_u32
 //   byte swap         v_perm_b32
 // so a round is 14 ops (4 for each big sigma, 1 choose, 1 majority, 2 adds
