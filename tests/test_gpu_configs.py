@@ -1,0 +1,214 @@
+"""GPU parity on the five workloads at full size, in the launch shapes bench.py
+uses (one hashing call per batch and mode, the table sizes of the configs).
+
+* tiny, paper, template: every digest, every hit count and n_new against the
+  oracle.
+* probe (8M resident keys, 1M probes): sampled requests' digests against the
+  oracle; every hit count against the value fixed by construction (d for a
+  probe copying d blocks under its own principal, 0 under another principal),
+  and for sampled probes against the oracle's own lookup in its source chain.
+* large (65,536 requests, 13.7M blocks per mode): sampled requests (including
+  the longest) against the oracle; at full size, properties that hold at any
+  size: all keys distinct so n_new equals the block count, and a lookup of the
+  inserted batch hits every block.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+K = pytest.importorskip("paper_2608_09225_amd.kvgov")
+PROCS = min(16, len(os.sched_getaffinity(0)))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    K.lib()
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def gpu_chains(b, salts_dev, mode):
+    return K.hash_chains(dev(b.tokens), dev(b.tok_offsets), dev(b.principal), salts_dev, mode,
+                         dev(b.boundary_tok))
+
+
+def oracle_chains(b, salts, mode, requests=None):
+    if requests is None:
+        return O.hash_chains_parallel(b.tokens, b.tok_offsets, b.principal, salts, mode,
+                                      b.boundary_tok, processes=PROCS)
+    return O.hash_chains(b.tokens, b.tok_offsets, b.principal, salts, mode, b.boundary_tok,
+                         requests=requests)
+
+
+_BO = {}
+
+
+def rows_of(b, hashes_np, r):
+    if id(b) not in _BO:
+        _BO[id(b)] = (b, b.blk_offsets())
+    bo = _BO[id(b)][1]
+    return hashes_np[bo[r]:bo[r + 1]]
+
+
+def full_pipeline(wl, mode):
+    """GPU: chains of both batches, insert, lookup.  Oracle: the same."""
+    sd = K.salts(wl.K, dev(wl.principal_ids))
+    osalts = O.salts(wl.K, wl.principal_ids)
+    assert sd.cpu().numpy().tobytes() == b"".join(osalts)
+    hi = gpu_chains(wl.insert, sd, mode)
+    hl = gpu_chains(wl.lookup, sd, mode)
+    with K.Cache(wl.log2_slots) as c:
+        n_new = c.insert(hi, dev(wl.insert.blk_offsets()))
+        hits = c.lookup(hl, dev(wl.lookup.blk_offsets())).cpu().numpy()
+        count = c.count()
+    wi = oracle_chains(wl.insert, osalts, mode)
+    wlk = oracle_chains(wl.lookup, osalts, mode)
+    assert np.array_equal(hi.cpu().numpy(), wi)
+    assert np.array_equal(hl.cpu().numpy(), wlk)
+    T = O.Table()
+    assert n_new == T.insert(wi) == count
+    want_hits = T.lookup(wlk, wl.lookup.blk_offsets())
+    assert np.array_equal(hits, want_hits)
+    return hits
+
+
+def test_tiny_config():
+    wl = W.make("tiny")
+    hits = full_pipeline(wl, W.ROOT)
+    assert np.array_equal(hits, wl.lookup.expect_hits[W.ROOT])
+
+
+@pytest.fixture(scope="module")
+def paper_wl():
+    return W.make("paper")
+
+
+@pytest.mark.parametrize("mode", [W.ROOT, W.BOUNDARY, W.NONE])
+def test_paper_config(paper_wl, mode):
+    wl = paper_wl
+    hits = full_pipeline(wl, mode)
+    assert np.array_equal(hits, wl.lookup.expect_hits[mode])  # 132 for every request
+
+
+def test_template_config():
+    """All three modes; the hit-block retention of boundary salting relative to
+    no salting is the same number on both sides (it is computed from hits that
+    are compared exactly)."""
+    wl = W.make("template")
+    hits = {m: full_pipeline(wl, m) for m in (W.NONE, W.ROOT, W.BOUNDARY)}
+    k = wl.notes["boundary_tok"] // 16
+    # by construction: every request shares the first k template blocks
+    assert np.all(hits[W.BOUNDARY] >= k) and np.all(hits[W.NONE] >= hits[W.BOUNDARY])
+    assert np.all(hits[W.ROOT] <= hits[W.NONE])
+    retention = hits[W.BOUNDARY].sum() / hits[W.NONE].sum()
+    assert 0 < retention <= 1
+
+
+@pytest.fixture(scope="module")
+def probe_wl():
+    return W.make("probe")
+
+
+def test_probe_config(probe_wl):
+    wl = probe_wl
+    res, pr = wl.insert, wl.lookup
+    sd = K.salts(wl.K, dev(wl.principal_ids))
+    osalts = O.salts(wl.K, wl.principal_ids)
+    h_res = gpu_chains(res, sd, W.ROOT)
+    h_pr = gpu_chains(pr, sd, W.ROOT)
+    with K.Cache(wl.log2_slots) as c:
+        assert c.slots() == 1 << 24
+        n_new = c.insert(h_res, dev(res.blk_offsets()))
+        hits = c.lookup(h_pr, dev(pr.blk_offsets())).cpu().numpy()
+    assert n_new == res.n * 32  # random 512-token prompts: every key distinct
+    assert np.array_equal(hits, pr.expect_hits[W.ROOT])
+    # sampled digests against the oracle
+    g = np.random.default_rng(5)
+    hr, hp = h_res.cpu().numpy(), h_pr.cpu().numpy()
+    for r in g.choice(res.n, 300, replace=False):
+        assert np.array_equal(rows_of(res, hr, r), oracle_chains(res, osalts, W.ROOT, [int(r)]))
+    for p in g.choice(pr.n, 300, replace=False):
+        assert np.array_equal(rows_of(pr, hp, p), oracle_chains(pr, osalts, W.ROOT, [int(p)]))
+
+
+def test_probe_sources_checked_by_oracle(probe_wl):
+    """For sampled own-principal probes, the oracle hashes the probe and the
+    resident request it was copied from and counts leading common keys."""
+    wl = probe_wl
+    res, pr = wl.insert, wl.lookup
+    osalts = O.salts(wl.K, wl.principal_ids)
+    L = 512
+    first_block = {res.tokens[L * r:L * r + 16].tobytes(): r for r in range(res.n)}
+    g = np.random.default_rng(6)
+    checked = 0
+    for p in g.choice(pr.n, 400, replace=False):
+        d = int(pr.expect_hits[W.ROOT][p])
+        if d == 0:
+            continue
+        # the source is the resident request whose first block equals the probe's
+        r = first_block[pr.row(int(p))[:16].tobytes()]
+        keys = set(bytes(x) for x in oracle_chains(res, osalts, W.ROOT, [r]))
+        ph = oracle_chains(pr, osalts, W.ROOT, [int(p)])
+        j = 0
+        while j < len(ph) and bytes(ph[j]) in keys:
+            j += 1
+        assert j == d
+        checked += 1
+    assert checked > 200
+
+
+@pytest.fixture(scope="module")
+def large_wl():
+    return W.make("large")
+
+
+@pytest.mark.parametrize("mode", [W.ROOT, W.BOUNDARY])
+def test_large_config(large_wl, mode):
+    wl = large_wl
+    b = wl.insert
+    sd = K.salts(wl.K, dev(wl.principal_ids))
+    osalts = O.salts(wl.K, wl.principal_ids)
+    h = gpu_chains(b, sd, mode)
+    nb = int(b.block_counts().sum())
+    with K.Cache(wl.log2_slots) as c:
+        assert c.insert(h, dev(b.blk_offsets())) == nb  # all keys distinct
+        hits = c.lookup(h, dev(b.blk_offsets())).cpu().numpy()
+    assert np.array_equal(hits, b.block_counts())
+    hn = h.cpu().numpy()
+    g = np.random.default_rng(7)
+    longest = np.argsort(-b.lengths)[:16]
+    sample = np.concatenate([longest, g.choice(b.n, 400, replace=False)])
+    for r in sample:
+        assert np.array_equal(rows_of(b, hn, r), oracle_chains(b, osalts, mode, [int(r)])), r
+
+
+def test_many_requests_longest_first_ordering():
+    """A batch above the longest-first threshold (40,000 short requests)."""
+    g = np.random.default_rng(8)
+    lens = g.integers(0, 200, 40000).astype(np.int64)
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    toks = g.integers(0, W.VOCAB, int(offs[-1]), dtype=np.int32)
+    prin = g.integers(0, 50, lens.size).astype(np.int32)
+    bt = np.floor(g.random(lens.size) * (lens + 1)).astype(np.int32)
+    b = W.Batch(toks, offs, prin, bt)
+    Kb = g.integers(0, 256, 32, dtype=np.uint8).tobytes()
+    ids = g.integers(0, 256, (50, 32), dtype=np.uint8)
+    sd = K.salts(Kb, dev(ids))
+    osalts = O.salts(Kb, ids)
+    for mode in (W.NONE, W.ROOT, W.BOUNDARY):
+        got = gpu_chains(b, sd, mode).cpu().numpy()
+        assert np.array_equal(got, oracle_chains(b, osalts, mode))
