@@ -41,12 +41,17 @@ namespace kvgov {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4), aligned(4)));
 
+// Counters are spread over kCounterLanes addresses (a workgroup adds to lane
+// blockIdx % kCounterLanes): atomics on one address serialise at ~10 ns each,
+// which at one atomic per wave dominated a 680k-key insert.  Readers sum.
+constexpr int kCounterLanes = 64;
+
 struct CacheMeta {
-  unsigned long long n_keys;       // keys in the table (all-0xFF key included)
-  unsigned long long new_keys[2];  // keys added by insert call `epoch`, at [epoch & 1]
-  unsigned long long exported;     // keys written by the latest export
-  int32_t status;                  // latched error (0 = none)
-  int32_t ones_present;            // the all-0xFF key is in the table
+  unsigned long long n_keys[kCounterLanes];       // keys in the table (all-0xFF key included)
+  unsigned long long new_keys[2][kCounterLanes];  // keys added by insert call `epoch`, at [epoch & 1]
+  unsigned long long exported;                    // keys written by the latest export
+  int32_t status;                                 // latched error (0 = none)
+  int32_t ones_present;                           // the all-0xFF key is in the table
 };
 
 struct TableView {
@@ -98,13 +103,17 @@ __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long l
                                                     int64_t slots, CacheMeta *m) {
   const int64_t stride = (int64_t)gridDim.x * 256;
   const u32x4 ones = u32x4{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    m->n_keys = 0;
-    m->new_keys[0] = 0;
-    m->new_keys[1] = 0;
-    m->exported = 0;
-    m->status = 0;
-    m->ones_present = 0;
+  if (blockIdx.x == 0) {
+    for (int i = threadIdx.x; i < kCounterLanes; i += blockDim.x) {
+      m->n_keys[i] = 0;
+      m->new_keys[0][i] = 0;
+      m->new_keys[1][i] = 0;
+    }
+    if (threadIdx.x == 0) {
+      m->exported = 0;
+      m->status = 0;
+      m->ones_present = 0;
+    }
   }
   for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < slots; s += stride) {
     keys[2 * s] = ones;
@@ -113,18 +122,13 @@ __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long l
   }
 }
 
-__device__ __forceinline__ void add_wave_count(unsigned long long *dst1,
-                                               unsigned long long *dst2, uint32_t v) {
-  // one atomic per wave: sum over the active lanes
-  const uint64_t active = __ballot(1);
-  uint32_t s = v;
+// Sum of v over the workgroup (256 threads), valid in thread 0.
+__device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t *lds4) {
 #pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) s += __shfl_xor(s, d, 64);
-  const int lane = threadIdx.x & 63;
-  if (lane == __builtin_ctzll(active) && s) {
-    atomicAdd(dst1, (unsigned long long)s);
-    if (dst2) atomicAdd(dst2, (unsigned long long)s);
-  }
+  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
+  if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return threadIdx.x == 0 ? lds4[0] + lds4[1] + lds4[2] + lds4[3] : 0;
 }
 
 // Tags only ever change from 0 to a claim, so a plain (possibly stale) read
@@ -133,9 +137,11 @@ __device__ __forceinline__ void add_wave_count(unsigned long long *dst1,
 __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hashes,
                                                 const int64_t *blk_offsets, int32_t n,
                                                 int64_t n_blocks, uint32_t epoch) {
+  __shared__ uint32_t lds4[4];
   const int64_t lo = blk_offsets[0], hi = blk_offsets[n];
   const bool first = blockIdx.x == 0 && threadIdx.x == 0;
-  if (first) t.meta->new_keys[(epoch + 1) & 1] = 0;  // counter of the next call
+  if (blockIdx.x == 0 && threadIdx.x < kCounterLanes)
+    t.meta->new_keys[(epoch + 1) & 1][threadIdx.x] = 0;  // counters of the next call
   if (lo < 0 || hi < lo || hi > n_blocks || hi - lo >= 0xFFFFFFFFll) {
     if (first) atomicCAS(&t.meta->status, 0, KVGOV_E_OFFSETS);
     return;
@@ -182,7 +188,12 @@ __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hash
       }
     }
   }
-  add_wave_count(&t.meta->new_keys[epoch & 1], &t.meta->n_keys, added);
+  const uint32_t total = block_sum(added, lds4);
+  if (threadIdx.x == 0 && total) {
+    const int lane = blockIdx.x % kCounterLanes;
+    atomicAdd(&t.meta->new_keys[epoch & 1][lane], (unsigned long long)total);
+    atomicAdd(&t.meta->n_keys[lane], (unsigned long long)total);
+  }
 }
 
 // Is `key` in the table?  Reads the key array only.
@@ -230,14 +241,42 @@ __global__ __launch_bounds__(256) void k_lookup(LookupArgs a) {
   const bool ones = a.t.meta->ones_present != 0;
   const int64_t nf = b1 - b0;
   int64_t hit = nf;
-  for (int64_t j0 = 0; j0 < nf; j0 += G) {
-    const int64_t j = j0 + sub;
-    bool miss = false;
-    if (j < nf) miss = !probe(a.t, load_key(a.hashes + (b0 + j) * 32), ones);
-    const uint64_t m = __ballot(miss) & gmask;
-    if (m) {
-      hit = j0 + (__builtin_ctzll(m) - base);
-      break;
+  if constexpr (G == 1) {
+    // One lane per request: its query keys are read a 128-byte line (four
+    // keys) at a time, so each line of the hashes array is fetched once
+    // instead of once per key.
+    int64_t j = 0;
+    bool stop = false;
+    while (!stop && j < nf) {
+      const int64_t idx = b0 + j;
+      const int64_t line = idx & ~(int64_t)3;
+      Key q[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        q[u] = (line + u < a.n_blocks) ? load_key(a.hashes + (line + u) * 32) : Key{};
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (!stop && line + u >= idx && j < nf) {
+          if (probe(a.t, q[u], ones)) {
+            ++j;
+          } else {
+            hit = j;
+            stop = true;
+          }
+        }
+      }
+    }
+  } else {
+    for (int64_t j0 = 0; j0 < nf; j0 += G) {
+      const int64_t j = j0 + sub;
+      bool miss = false;
+      if (j < nf) miss = !probe(a.t, load_key(a.hashes + (b0 + j) * 32), ones);
+      const uint64_t m = __ballot(miss) & gmask;
+      if (m) {
+        hit = j0 + (__builtin_ctzll(m) - base);
+        break;
+      }
     }
   }
   if (sub == 0) a.hit_blocks[r] = (int32_t)hit;
@@ -245,26 +284,44 @@ __global__ __launch_bounds__(256) void k_lookup(LookupArgs a) {
 
 __global__ void k_export_begin(CacheMeta *m) { m->exported = 0; }
 
+// One atomic per wave reserves the output rows of the wave's keys.
+__device__ __forceinline__ void export_key(bool have, const u32x4 &lo, const u32x4 &hi,
+                                           CacheMeta *m, uint8_t *out, int64_t cap) {
+  const uint64_t mask = __ballot(have);
+  if (!mask) return;
+  const int lane = threadIdx.x & 63;
+  const int leader = __builtin_ctzll(mask);
+  unsigned long long base = 0;
+  if (lane == leader) base = atomicAdd(&m->exported, (unsigned long long)__popcll(mask));
+  base = __shfl(base, leader, 64);
+  if (have) {
+    const int64_t at = (int64_t)base + __popcll(mask & ((1ull << lane) - 1ull));
+    if (at < cap) {
+      u32x4 *q = reinterpret_cast<u32x4 *>(out + at * 32);
+      q[0] = lo;
+      q[1] = hi;
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void k_export(TableView t, uint8_t *out, int64_t cap) {
   const int64_t stride = (int64_t)gridDim.x * 256;
   const int64_t slots = (int64_t)t.mask + 1;
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (gid == 0 && t.meta->ones_present) {
-    const unsigned long long at = atomicAdd(&t.meta->exported, 1ull);
-    if ((int64_t)at < cap) {
-      u32x4 *q = reinterpret_cast<u32x4 *>(out + at * 32);
-      q[0] = u32x4{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
-      q[1] = q[0];
+  const u32x4 ones = u32x4{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+  if (blockIdx.x == 0 && threadIdx.x < 64)
+    export_key(threadIdx.x == 0 && t.meta->ones_present != 0, ones, ones, t.meta, out, cap);
+  // every lane of a wave runs the same number of iterations (ballot inside)
+  const int64_t rounds = (slots + stride - 1) / stride;
+  for (int64_t k = 0; k < rounds; ++k) {
+    const int64_t s = gid + k * stride;
+    const bool have = s < slots && t.tags[s] != 0;
+    u32x4 lo = ones, hi = ones;
+    if (have) {
+      lo = t.keys[2 * s];
+      hi = t.keys[2 * s + 1];
     }
-  }
-  for (int64_t s = gid; s < slots; s += stride) {
-    if (t.tags[s] == 0) continue;
-    const unsigned long long at = atomicAdd(&t.meta->exported, 1ull);
-    if ((int64_t)at < cap) {
-      u32x4 *q = reinterpret_cast<u32x4 *>(out + at * 32);
-      q[0] = t.keys[2 * s];
-      q[1] = t.keys[2 * s + 1];
-    }
+    export_key(have, lo, hi, t.meta, out, cap);
   }
 }
 
@@ -389,7 +446,9 @@ int kvgov_cache_insert(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
   CacheMeta m{};
   rc = read_meta(c, &m, s);
   if (rc != KVGOV_OK) return rc;
-  *n_new = (int64_t)m.new_keys[epoch & 1];
+  int64_t added = 0;
+  for (int i = 0; i < kCounterLanes; ++i) added += (int64_t)m.new_keys[epoch & 1][i];
+  *n_new = added;
   return m.status;
 }
 
@@ -433,7 +492,9 @@ int kvgov_cache_count(kvgov_cache *c, int64_t *n_keys, void *stream) {
   CacheMeta m{};
   rc = read_meta(c, &m, as_stream(stream));
   if (rc != KVGOV_OK) return rc;
-  *n_keys = (int64_t)m.n_keys;
+  int64_t total = 0;
+  for (int i = 0; i < kCounterLanes; ++i) total += (int64_t)m.n_keys[i];
+  *n_keys = total;
   return m.status;
 }
 

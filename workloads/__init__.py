@@ -293,7 +293,7 @@ def probe(seed: int = SEED, n_res: int = 250_000, n_probe: int = 1_000_000,
     probes = Batch(toks, offs, prin.astype(np.int32),
                    np.zeros(n_probe, dtype=np.int32), {ROOT: hits})
     return Workload("probe", K, ids, resident, probes, [ROOT], 24,
-                    {"own_fraction": float(own.mean())})
+                    {"own_fraction": float(own.mean()), "source": src, "depth": d})
 
 
 def large(seed: int = SEED, n: int = 65536, P: int = 4096,
