@@ -264,10 +264,28 @@ __device__ __forceinline__ int order_bucket(const int64_t *tok_offsets, int32_t 
   return (int)(nb < kOrderBuckets - 1 ? nb : kOrderBuckets - 1);
 }
 
-__global__ __launch_bounds__(256) void k_order_hist(const int64_t *tok_offsets, int32_t n,
-                                                    int32_t *hist) {
-  const int32_t r = blockIdx.x * 256 + threadIdx.x;
-  if (r < n) atomicAdd(&hist[order_bucket(tok_offsets, r)], 1);
+// Histogram and scatter work on tiles of kOrderTile requests per workgroup and
+// count in LDS first, so global atomics are one per (tile, non-empty bucket):
+// per-request atomics on a few hot bucket counters serialise (4 ms for a
+// 1.25M-request batch).
+constexpr int kOrderThreads = 1024;
+constexpr int kOrderPerThread = 4;
+constexpr int64_t kOrderTile = (int64_t)kOrderThreads * kOrderPerThread;
+
+__global__ __launch_bounds__(kOrderThreads) void k_order_hist(const int64_t *tok_offsets,
+                                                              int32_t n, int32_t *hist) {
+  __shared__ int32_t h[kOrderBuckets];
+  for (int i = threadIdx.x; i < kOrderBuckets; i += kOrderThreads) h[i] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * kOrderTile;
+#pragma unroll
+  for (int k = 0; k < kOrderPerThread; ++k) {
+    const int64_t r = base + (int64_t)k * kOrderThreads + threadIdx.x;
+    if (r < n) atomicAdd(&h[order_bucket(tok_offsets, (int32_t)r)], 1);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < kOrderBuckets; i += kOrderThreads)
+    if (h[i]) atomicAdd(&hist[i], h[i]);
 }
 
 // one workgroup: start[b] = number of requests in buckets above b (descending order)
@@ -275,8 +293,8 @@ __global__ __launch_bounds__(256) void k_order_scan(int32_t *hist) {
   __shared__ int32_t sums[256];
   constexpr int per = kOrderBuckets / 256;
   const int t = threadIdx.x;
-  // thread t owns buckets [kOrderBuckets - per*(t+1), kOrderBuckets - per*t)
-  // i.e. the highest buckets go to thread 0
+  // thread t owns buckets kOrderBuckets-1-t*per down to kOrderBuckets-(t+1)*per,
+  // so the highest buckets go to thread 0
   int32_t local = 0;
   for (int i = 0; i < per; ++i) local += hist[kOrderBuckets - 1 - (t * per + i)];
   sums[t] = local;
@@ -292,10 +310,35 @@ __global__ __launch_bounds__(256) void k_order_scan(int32_t *hist) {
   }
 }
 
-__global__ __launch_bounds__(256) void k_order_scatter(const int64_t *tok_offsets, int32_t n,
-                                                       int32_t *cursor, int32_t *order) {
-  const int32_t r = blockIdx.x * 256 + threadIdx.x;
-  if (r < n) order[atomicAdd(&cursor[order_bucket(tok_offsets, r)], 1)] = r;
+__global__ __launch_bounds__(kOrderThreads) void k_order_scatter(const int64_t *tok_offsets,
+                                                                 int32_t n, int32_t *cursor,
+                                                                 int32_t *order) {
+  __shared__ int32_t cnt[kOrderBuckets];
+  __shared__ int32_t at[kOrderBuckets];
+  for (int i = threadIdx.x; i < kOrderBuckets; i += kOrderThreads) cnt[i] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * kOrderTile;
+  int32_t bucket[kOrderPerThread], rank[kOrderPerThread];
+#pragma unroll
+  for (int k = 0; k < kOrderPerThread; ++k) {
+    const int64_t r = base + (int64_t)k * kOrderThreads + threadIdx.x;
+    bucket[k] = -1;
+    if (r < n) {
+      bucket[k] = order_bucket(tok_offsets, (int32_t)r);
+      rank[k] = atomicAdd(&cnt[bucket[k]], 1);
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < kOrderBuckets; i += kOrderThreads)
+    if (cnt[i]) at[i] = atomicAdd(&cursor[i], cnt[i]);
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < kOrderPerThread; ++k) {
+    if (bucket[k] >= 0) {
+      const int64_t r = base + (int64_t)k * kOrderThreads + threadIdx.x;
+      order[at[bucket[k]] + rank[k]] = (int32_t)r;
+    }
+  }
 }
 
 __global__ __launch_bounds__(256) void k_fill_i32(int32_t *p, int64_t count, int32_t v) {
@@ -588,11 +631,11 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
     int32_t *order = scratch + kOrderBuckets;
     hipLaunchKernelGGL(k_fill_i32, dim3(kOrderBuckets / 256), dim3(256), 0, s, hist,
                        (int64_t)kOrderBuckets, 0);
-    hipLaunchKernelGGL(k_order_hist, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, s,
-                       tok_offsets, n, hist);
+    const dim3 tiles((unsigned)ceil_div(n, kOrderTile));
+    hipLaunchKernelGGL(k_order_hist, tiles, dim3(kOrderThreads), 0, s, tok_offsets, n, hist);
     hipLaunchKernelGGL(k_order_scan, dim3(1), dim3(256), 0, s, hist);
-    hipLaunchKernelGGL(k_order_scatter, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, s,
-                       tok_offsets, n, hist, order);
+    hipLaunchKernelGGL(k_order_scatter, tiles, dim3(kOrderThreads), 0, s, tok_offsets, n, hist,
+                       order);
     a.order = order;
   }
   // Launch shape.  A chain wave is bound by its SIMD's issue rate, so it
