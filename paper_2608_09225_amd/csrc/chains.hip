@@ -37,6 +37,13 @@
 #include "common.h"
 #include "sha256_cdna4.h"
 
+#ifndef KVGOV_PAIR_DEFAULT
+#define KVGOV_PAIR_DEFAULT 1
+#endif
+#ifndef KVGOV_PAIRS
+#define KVGOV_PAIRS 1
+#endif
+
 namespace kvgov {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4), aligned(4)));
@@ -366,112 +373,456 @@ struct ChainArgs {
   int32_t *status;
 };
 
+// Per-request set-up shared by both chain kernels.  Returns false (after
+// latching the error) for a request that must write nothing.
+struct ChainReq {
+  const int32_t *tp;  // first token
+  uint8_t *out;       // first output row
+  int64_t nf;         // full blocks
+  int64_t k;          // salted block (boundary mode), else -1
+  uint32_t sig[8];    // salt as state words (salted modes)
+  bool salted_root;   // first block carries the salt (root, or boundary k = 0)
+};
+
+template <int MODE>
+__device__ __forceinline__ bool chain_setup(const ChainArgs &a, int32_t r, ChainReq &q) {
+  const int64_t t0 = a.tok_offsets[r], t1 = a.tok_offsets[r + 1];
+  if (t0 < 0 || t1 < t0 || t1 > a.n_tokens) {
+    latch(a.status, KVGOV_E_OFFSETS);
+    return false;
+  }
+  const int64_t len = t1 - t0;
+  q.nf = len >> 4;
+  const int64_t b0 = a.blk_offsets[r];
+  if (b0 < 0 || a.blk_offsets[r + 1] - b0 != q.nf || b0 + q.nf > a.n_blocks) {
+    latch(a.status, KVGOV_E_OFFSETS);
+    return false;
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) q.sig[i] = 0;
+  if (MODE != KVGOV_NONE) {
+    const int32_t p = a.principal[r];
+    if (p < 0 || p >= a.P) {
+      latch(a.status, KVGOV_E_PRINCIPAL);
+      return false;
+    }
+    load_digest(a.salts + (int64_t)p * 32, q.sig);
+  }
+  q.k = -1;
+  if (MODE == KVGOV_BOUNDARY) {
+    const int32_t bt = a.boundary_tok[r];
+    if (bt < 0 || bt > len) {
+      latch(a.status, KVGOV_E_BOUNDARY);
+      return false;
+    }
+    q.k = bt >> 4;
+  }
+  q.tp = a.tokens + t0;
+  q.out = a.hashes + b0 * 32;
+  q.salted_root = (MODE == KVGOV_ROOT) || (MODE == KVGOV_BOUNDARY && q.k == 0);
+  return true;
+}
+
+// The special path, per lane (rolled compressions):
+//   normal  : (IV; h || T[0..7])        (state; T[8..15] || pad96)
+//   u0      : (IV; T[0..15])            (state; pad64)
+//   boundary: (IV; sigma || h) -> X,   (X; T[0..15])   (state; pad128)
+// H (h_{j-1} in, h_j out) and the block's token words T.
+__device__ __forceinline__ void special_block(uint32_t H[8], const uint32_t T[16],
+                                              const uint32_t sig[8], bool u0, bool bnd) {
+  uint32_t X[8], st[8], w[16];
+  set_iv(X);
+  if (bnd) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) { w[q] = sig[q]; w[8 + q] = H[q]; }
+    compress_rolled(X, w);
+  }
+  const bool whole = u0 || bnd;  // first compression takes all 16 token words
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    st[q] = X[q];
+    w[q] = whole ? T[q] : H[q];
+    w[8 + q] = whole ? T[8 + q] : T[q];
+  }
+  compress_rolled(st, w);
+#pragma unroll
+  for (int q = 0; q < 8; ++q) w[q] = whole ? (q == 0 ? 0x80000000u : 0u) : T[8 + q];
+  w[8] = whole ? 0u : 0x80000000u;
+#pragma unroll
+  for (int q = 9; q < 15; ++q) w[q] = 0;
+  w[15] = u0 ? 64 * 8 : (bnd ? 128 * 8 : 96 * 8);
+  compress_rolled(st, w);
+#pragma unroll
+  for (int q = 0; q < 8; ++q) H[q] = st[q];
+}
+
+// Padding words 8..15 of the second block of a 96-byte message.
+__device__ __forceinline__ void pad96_tail(uint32_t w[16]) {
+  w[8] = 0x80000000u;
+#pragma unroll
+  for (int q = 9; q < 15; ++q) w[q] = 0;
+  w[15] = 96 * 8;
+}
+
+// One lane per request.  Every instruction of a compression (rounds and
+// message schedule) is issued by the lane's wave.
 template <int MODE>
 __global__ __launch_bounds__(256) void k_chains(ChainArgs a) {
   const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.n) return;
   const int32_t r = a.order ? a.order[i] : i;
-
-  // ---- validate this request; a rejected request writes nothing
-  const int64_t t0 = a.tok_offsets[r], t1 = a.tok_offsets[r + 1];
-  if (t0 < 0 || t1 < t0 || t1 > a.n_tokens) {
-    latch(a.status, KVGOV_E_OFFSETS);
-    return;
-  }
-  const int64_t len = t1 - t0;
-  const int64_t nf = len >> 4;
-  const int64_t b0 = a.blk_offsets[r];
-  if (b0 < 0 || a.blk_offsets[r + 1] - b0 != nf || b0 + nf > a.n_blocks) {
-    latch(a.status, KVGOV_E_OFFSETS);
-    return;
-  }
-  uint32_t sig[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  if (MODE != KVGOV_NONE) {
-    const int32_t p = a.principal[r];
-    if (p < 0 || p >= a.P) {
-      latch(a.status, KVGOV_E_PRINCIPAL);
-      return;
-    }
-    load_digest(a.salts + (int64_t)p * 32, sig);
-  }
-  int64_t k = -1;  // salted block (boundary mode)
-  if (MODE == KVGOV_BOUNDARY) {
-    const int32_t bt = a.boundary_tok[r];
-    if (bt < 0 || bt > len) {
-      latch(a.status, KVGOV_E_BOUNDARY);
-      return;
-    }
-    k = bt >> 4;
-  }
-  if (nf == 0) return;
-
-  const int32_t *tp = a.tokens + t0;
-  uint8_t *out = a.hashes + b0 * 32;
+  ChainReq q;
+  if (!chain_setup<MODE>(a, r, q) || q.nf == 0) return;
+  const int64_t nf = q.nf;
 
   // H holds h_{j-1} as state words; a root-salted first block (and k == 0 in
   // boundary mode) is the usual pattern with sigma in place of h_{-1}.
   uint32_t H[8];
-  const bool salted_root = (MODE == KVGOV_ROOT) || (MODE == KVGOV_BOUNDARY && k == 0);
 #pragma unroll
-  for (int q = 0; q < 8; ++q) H[q] = salted_root ? sig[q] : 0u;
+  for (int w = 0; w < 8; ++w) H[w] = q.salted_root ? q.sig[w] : 0u;
 
   u32x4 nxt[4];
-  load_raw(tp, nxt);
-  // special-path flags: unsalted 64-byte first block, boundary block
-  const bool plain_first = !salted_root;
+  load_raw(q.tp, nxt);
+  const bool plain_first = !q.salted_root;
 
   for (int64_t j = 0; j < nf; ++j) {
     uint32_t T[16];
     swap_block(nxt, T);
-    if (j + 1 < nf) load_raw(tp + 16 * (j + 1), nxt);
+    if (j + 1 < nf) load_raw(q.tp + 16 * (j + 1), nxt);
 
     const bool u0 = plain_first && j == 0;
-    const bool bnd = (MODE == KVGOV_BOUNDARY) && j == k && k > 0;
-    uint32_t st[8], w[16];
+    const bool bnd = (MODE == KVGOV_BOUNDARY) && j == q.k && q.k > 0;
     if (MODE == KVGOV_ROOT || !__any(u0 || bnd)) {
       // hot path: (IV; h || T[0..7]) then (state; T[8..15] || pad96)
+      uint32_t st[8], w[16];
       set_iv(st);
 #pragma unroll
-      for (int q = 0; q < 8; ++q) { w[q] = H[q]; w[8 + q] = T[q]; }
+      for (int x = 0; x < 8; ++x) { w[x] = H[x]; w[8 + x] = T[x]; }
       compress(st, w);
 #pragma unroll
-      for (int q = 0; q < 8; ++q) w[q] = T[8 + q];
-      w[8] = 0x80000000u;
-#pragma unroll
-      for (int q = 9; q < 15; ++q) w[q] = 0;
-      w[15] = 96 * 8;
+      for (int x = 0; x < 8; ++x) w[x] = T[8 + x];
+      pad96_tail(w);
       compress(st, w);
+#pragma unroll
+      for (int x = 0; x < 8; ++x) H[x] = st[x];
     } else {
-      // special path, per lane:
-      //   normal  : (IV; h || T[0..7])        (state; T[8..15] || pad96)
-      //   u0      : (IV; T[0..15])            (state; pad64)
-      //   boundary: (IV; sigma || h) -> X,   (X; T[0..15])   (state; pad128)
-      uint32_t X[8];
-      set_iv(X);
-      if (bnd) {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) { w[q] = sig[q]; w[8 + q] = H[q]; }
-        compress_rolled(X, w);
-      }
-      const bool whole = u0 || bnd;  // first compression takes all 16 token words
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        st[q] = X[q];
-        w[q] = whole ? T[q] : H[q];
-        w[8 + q] = whole ? T[8 + q] : T[q];
-      }
-      compress_rolled(st, w);
-#pragma unroll
-      for (int q = 0; q < 8; ++q) w[q] = whole ? (q == 0 ? 0x80000000u : 0u) : T[8 + q];
-      w[8] = whole ? 0u : 0x80000000u;
-#pragma unroll
-      for (int q = 9; q < 15; ++q) w[q] = 0;
-      w[15] = u0 ? 64 * 8 : (bnd ? 128 * 8 : 96 * 8);
-      compress_rolled(st, w);
+      special_block(H, T, q.sig, u0, bnd);
     }
+    store_digest(q.out + j * 32, H);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// wave-pair chain kernel
+// ---------------------------------------------------------------------------
+//
+// A chain is latency-bound: one wave advances 64 chains at the issue rate of
+// its SIMD, and a block costs ~2800 vector instructions, a third of them the
+// message schedule.  The schedule does not feed back into the rounds except
+// through its output words, so a second wave on another SIMD computes it and
+// hands the words over through LDS:
+//   wave 0 ("rounds")   : the 64 rounds of each compression, state in registers;
+//   wave 1 ("schedule") : W[16..63] of both compressions of every block.
+// Lane l of both waves owns the same request.  Per block j:
+//   phase 1  rounds: C1 rounds 0-15 (message h_{j-1} || T[0..7] in registers)
+//            schedule: reads h_{j-1} from LDS, computes C1's W[16..31]
+//   phase 2  rounds: C1 rounds 16-31       schedule: C1's W[32..47]
+//   phase 3  rounds: C1 rounds 32-47       schedule: C1's W[48..63]
+//   phase 4  rounds: C1 rounds 48-63, then all of C2 (its W[16..63] were
+//            computed during block j-1: the C2 message T[8..15] || padding
+//            depends on tokens only); writes h_j to LDS and the digest
+//            schedule: C2's W[16..63] of block j+1 (double buffered)
+// with a workgroup barrier after each phase.  Iterations where a lane of the
+// wave has a special block (unsalted first block, boundary block) run the
+// special path entirely on the rounds wave; the schedule wave then only
+// prepares the next block's C2 words.  Both waves derive every branch and
+// trip count from the same per-lane data, so they meet the same barriers.
+
+struct PairLds {
+  uint32_t h[8][kWave];          // h_{j-1} per lane
+  uint32_t w1[48][kWave];        // C1's W[16..63]
+  uint32_t w2[2][48][kWave];     // C2's W[16..63], double buffered by block parity
+};
+
+struct Sha8 {
+  uint32_t a, b, c, d, e, f, g, h;
+};
+
+__device__ __forceinline__ void round_w(Sha8 &s, uint32_t kt, uint32_t w) {
+  const uint32_t t1 = s.h + big_sigma1(s.e) + ch(s.e, s.f, s.g) + kt + w;
+  const uint32_t t2 = big_sigma0(s.a) + maj(s.a, s.b, s.c);
+  s.h = s.g; s.g = s.f; s.f = s.e; s.e = s.d + t1;
+  s.d = s.c; s.c = s.b; s.b = s.a; s.a = t1 + t2;
+}
+
+__device__ __forceinline__ Sha8 sha8_iv() {
+  return Sha8{kSha.H0[0], kSha.H0[1], kSha.H0[2], kSha.H0[3],
+              kSha.H0[4], kSha.H0[5], kSha.H0[6], kSha.H0[7]};
+}
+
+__device__ __forceinline__ Sha8 sha8_load(const uint32_t st[8]) {
+  return Sha8{st[0], st[1], st[2], st[3], st[4], st[5], st[6], st[7]};
+}
+
+__device__ __forceinline__ void sha8_add(uint32_t st[8], const Sha8 &s) {
+  st[0] += s.a; st[1] += s.b; st[2] += s.c; st[3] += s.d;
+  st[4] += s.e; st[5] += s.f; st[6] += s.g; st[7] += s.h;
+}
+
+// 16 schedule words from LDS into registers
+__device__ __forceinline__ void load16(uint32_t w[16], const uint32_t (*wl)[kWave], int base,
+                                       int lane) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) H[q] = st[q];
-    store_digest(out + j * 32, H);
+  for (int i = 0; i < 16; ++i) w[i] = wl[base + i][lane];
+}
+
+// rounds t0..t0+11 and t0..t0+3 with W[t0 + i] = w[i]
+__device__ __forceinline__ void rounds12(Sha8 &s, const uint32_t *w, int t0) {
+#pragma unroll
+  for (int i = 0; i < 12; ++i) round_w(s, kSha.K[t0 + i], w[i]);
+}
+__device__ __forceinline__ void rounds4(Sha8 &s, const uint32_t *w, int t0) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) round_w(s, kSha.K[t0 + i], w[i]);
+}
+
+// 16 schedule words W[t..t+15] from the rolling window w (W[t-16..t-1]),
+// stored to out[base + i][lane]
+__device__ __forceinline__ void sched16(uint32_t w[16], uint32_t (*out)[kWave], int base,
+                                        int lane) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    w[i] = small_sigma1(w[(i + 14) & 15]) + w[(i + 9) & 15] + small_sigma0(w[(i + 1) & 15]) +
+           w[i];
+    out[base + i][lane] = w[i];
+  }
+}
+
+// Block-count summary of a request used to keep the waves of a workgroup in
+// lockstep: every wave evaluates it for every pair's request of its lane.
+struct PairPeek {
+  int64_t nf;
+  int64_t k;
+  bool plain_first;
+};
+
+template <int MODE>
+__device__ __forceinline__ PairPeek pair_peek(const ChainArgs &a, int32_t i) {
+  PairPeek p{0, -1, false};
+  if (i < a.n) {
+    ChainReq q;
+    const int32_t r = a.order ? a.order[i] : i;
+    if (chain_setup<MODE>(a, r, q)) p = PairPeek{q.nf, q.k, !q.salted_root};
+  }
+  return p;
+}
+
+template <int MODE>
+__device__ __forceinline__ bool pair_special(const PairPeek &p, int64_t j) {
+  const bool act = j < p.nf;
+  return act && ((p.plain_first && j == 0) ||
+                 ((MODE == KVGOV_BOUNDARY) && j == p.k && p.k > 0));
+}
+
+// PAIRS wave pairs per workgroup: waves 2p (rounds) and 2p+1 (schedule) of
+// pair p own the 64 requests blockIdx.x * 64 * PAIRS + 64 p + lane.  Trip
+// count and special iterations are decided over all pairs of the workgroup,
+// so every wave meets every barrier.
+template <int MODE, int PAIRS>
+__global__ __launch_bounds__(2 * PAIRS * kWave) void k_chains_pair(ChainArgs a) {
+  __shared__ PairLds Lp[PAIRS];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int pair = wave >> 1;
+  const bool rounds_wave = (wave & 1) == 0;
+  PairLds &L = Lp[pair];
+  const int32_t base = blockIdx.x * kWave * PAIRS;
+  const int32_t i = base + pair * kWave + lane;
+
+  // identical set-up on both waves of a pair; a rejected or empty request
+  // has nf = 0 (both waves latch the same error, the first one wins)
+  ChainReq q;
+  bool ok = false;
+  if (i < a.n) {
+    const int32_t r = a.order ? a.order[i] : i;
+    ok = chain_setup<MODE>(a, r, q);
+  }
+  const int64_t nf = ok ? q.nf : 0;
+  PairPeek peek[PAIRS];
+#pragma unroll
+  for (int p = 0; p < PAIRS; ++p)
+    peek[p] = (p == pair) ? PairPeek{nf, ok ? q.k : -1, ok && !q.salted_root}
+                          : pair_peek<MODE>(a, base + p * kWave + lane);
+  // workgroup-uniform trip count
+  int64_t J = 0;
+#pragma unroll
+  for (int p = 0; p < PAIRS; ++p) J = peek[p].nf > J ? peek[p].nf : J;
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) {
+    const int64_t o = __shfl_xor(J, d, kWave);
+    J = o > J ? o : J;
+  }
+  const bool plain_first = ok && !q.salted_root;
+
+  uint32_t H[8];
+#pragma unroll
+  for (int w = 0; w < 8; ++w) H[w] = (ok && q.salted_root) ? q.sig[w] : 0u;
+
+  u32x4 nxt[4];    // tokens of the next block (both waves)
+  uint32_t T[16];  // tokens of the current block
+  if (nf > 0) load_raw(q.tp, nxt);
+
+  // prologue: h_{-1} to LDS; the schedule wave prepares C2's words of block 0
+  if (rounds_wave) {
+#pragma unroll
+    for (int w = 0; w < 8; ++w) L.h[w][lane] = H[w];
+  } else if (nf > 0) {
+    uint32_t T0[16];
+    swap_block(nxt, T0);
+    uint32_t w[16];
+#pragma unroll
+    for (int x = 0; x < 8; ++x) w[x] = T0[8 + x];
+    pad96_tail(w);
+    sched16(w, L.w2[0], 0, lane);
+    sched16(w, L.w2[0], 16, lane);
+    sched16(w, L.w2[0], 32, lane);
+  }
+  __syncthreads();
+
+  for (int64_t j = 0; j < J; ++j) {
+    const bool act = j < nf;
+    if (act) {
+      swap_block(nxt, T);
+      if (j + 1 < nf) load_raw(q.tp + 16 * (j + 1), nxt);
+    }
+    const bool u0 = act && plain_first && j == 0;
+    const bool bnd = act && (MODE == KVGOV_BOUNDARY) && j == q.k && q.k > 0;
+    const int nb = (int)((j + 1) & 1);  // C2 buffer of block j+1
+    const bool next = j + 1 < nf;
+
+    bool special_any = false;
+    if (MODE != KVGOV_ROOT) {
+#pragma unroll
+      for (int p = 0; p < PAIRS; ++p) special_any |= pair_special<MODE>(peek[p], j);
+    }
+    if (MODE != KVGOV_ROOT && __any(special_any)) {
+      // special iteration: the rounds wave does the whole block itself
+      if (rounds_wave) {
+        if (act) {
+          special_block(H, T, q.sig, u0, bnd);
+#pragma unroll
+          for (int w = 0; w < 8; ++w) L.h[w][lane] = H[w];
+          store_digest(q.out + j * 32, H);
+        }
+      } else if (next) {
+        uint32_t Tn[16], w[16];
+        swap_block(nxt, Tn);
+#pragma unroll
+        for (int x = 0; x < 8; ++x) w[x] = Tn[8 + x];
+        pad96_tail(w);
+        sched16(w, L.w2[nb], 0, lane);
+        sched16(w, L.w2[nb], 16, lane);
+        sched16(w, L.w2[nb], 32, lane);
+      }
+      __syncthreads();
+      continue;
+    }
+
+    if (rounds_wave) {
+      // Each barrier sits 4 rounds before the words it releases are needed,
+      // so the LDS reads issued right after it overlap those 4 rounds; the
+      // scheduling barriers keep the compiler from sinking the reads to
+      // their uses.  C2's words (written during the previous block) are read
+      // one group ahead.
+      Sha8 s = sha8_iv();
+      uint32_t wa[16], wb[16];
+      if (act) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) round_w(s, kSha.K[t], H[t]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) round_w(s, kSha.K[8 + t], T[t]);
+      }
+      __syncthreads();  // C1 W[16..31] ready
+      if (act) {
+        load16(wa, L.w1, 0, lane);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 4; t < 8; ++t) round_w(s, kSha.K[8 + t], T[t]);
+        rounds12(s, wa, 16);
+      }
+      __syncthreads();  // C1 W[32..47] ready
+      if (act) {
+        load16(wb, L.w1, 16, lane);
+        __builtin_amdgcn_sched_barrier(0);
+        rounds4(s, wa + 12, 28);
+        rounds12(s, wb, 32);
+      }
+      __syncthreads();  // C1 W[48..63] ready
+      if (act) {
+        const uint32_t(*w2)[kWave] = L.w2[j & 1];
+        load16(wa, L.w1, 32, lane);
+        __builtin_amdgcn_sched_barrier(0);
+        rounds4(s, wb + 12, 44);
+        load16(wb, w2, 0, lane);  // C2 W[16..31]
+        __builtin_amdgcn_sched_barrier(0);
+        rounds12(s, wa, 48);
+        rounds4(s, wa + 12, 60);
+        uint32_t st[8];
+#pragma unroll
+        for (int w = 0; w < 8; ++w) st[w] = kSha.H0[w];
+        sha8_add(st, s);
+        // C2: rounds 0-15 from registers (T[8..15] || pad96), 16-63 from LDS
+        Sha8 s2 = sha8_load(st);
+        load16(wa, w2, 16, lane);  // C2 W[32..47]
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) round_w(s2, kSha.K[t], T[8 + t]);
+        round_w(s2, kSha.K[8], 0x80000000u);
+#pragma unroll
+        for (int t = 9; t < 15; ++t) round_w(s2, kSha.K[t], 0u);
+        round_w(s2, kSha.K[15], 96 * 8);
+        rounds12(s2, wb, 16);
+        rounds4(s2, wb + 12, 28);
+        load16(wb, w2, 32, lane);  // C2 W[48..63]
+        __builtin_amdgcn_sched_barrier(0);
+        rounds12(s2, wa, 32);
+        rounds4(s2, wa + 12, 44);
+        rounds12(s2, wb, 48);
+        rounds4(s2, wb + 12, 60);
+        sha8_add(st, s2);
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+          H[w] = st[w];
+          L.h[w][lane] = st[w];
+        }
+        store_digest(q.out + j * 32, H);
+      }
+      __syncthreads();
+    } else {
+      // ---- schedule wave
+      uint32_t w[16];
+      if (act) {
+#pragma unroll
+        for (int x = 0; x < 8; ++x) { w[x] = L.h[x][lane]; w[8 + x] = T[x]; }
+        sched16(w, L.w1, 0, lane);
+      }
+      __syncthreads();
+      if (act) sched16(w, L.w1, 16, lane);
+      __syncthreads();
+      if (act) sched16(w, L.w1, 32, lane);
+      __syncthreads();
+      if (next) {
+        uint32_t Tn[16];
+        swap_block(nxt, Tn);
+#pragma unroll
+        for (int x = 0; x < 8; ++x) w[x] = Tn[8 + x];
+        pad96_tail(w);
+        sched16(w, L.w2[nb], 0, lane);
+        sched16(w, L.w2[nb], 16, lane);
+        sched16(w, L.w2[nb], 32, lane);
+      }
+      __syncthreads();
+    }
   }
 }
 
@@ -498,6 +849,39 @@ static size_t chain_lds_reserve() {
     per_dev[dev] = std::min<size_t>((size_t)cu_lds / 2 + 4096, (size_t)blk_lds);
   }
   return per_dev[dev];
+}
+
+static int cu_lds_bytes() {
+  int dev = 0, v = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+          hipSuccess ||
+      v <= 0)
+    v = 160 * 1024;
+  return v;
+}
+
+// Dynamic LDS of a wave-pair workgroup so that at most `per_cu` pair
+// workgroups share a CU (1: more than half of the CU's LDS; 2: more than a
+// third, at most half).
+static size_t pair_lds_reserve(int per_cu) {
+  const size_t cu = (size_t)cu_lds_bytes();
+  const size_t want = per_cu == 1 ? cu / 2 + 4096 : cu / 2 - 1024;
+  const size_t fixed = KVGOV_PAIRS * sizeof(PairLds);
+  return want > fixed ? want - fixed : 0;
+}
+
+// Pair workgroups per CU for a batch of n requests: the wave-pair kernel
+// shortens every chain but needs two waves per 64 requests, so it runs while
+// the batch fits in one or two pairs per CU (latency-bound batches); larger
+// batches keep every SIMD busy with the single-wave kernel (0).
+static int pair_slots(int32_t n) {
+  if (!KVGOV_PAIR_DEFAULT || n <= 0) return 0;
+  const int64_t pairs = ceil_div(n, (int64_t)kWave * KVGOV_PAIRS);
+  const int64_t cus = device_cu_count();
+  if (pairs <= cus) return 1;
+  if (pairs <= 2 * cus) return 2;
+  return 0;
 }
 
 int device_cu_count() {
@@ -641,18 +1025,30 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
   // Launch shape.  A chain wave is bound by its SIMD's issue rate, so it
   // should never share a SIMD while others sit idle.  The dispatcher stacks
   // the waves of concurrent launches on the same SIMDs, and the older wave
-  // then takes nearly every issue slot, so the workgroup reserves more than
-  // half of a CU's LDS (unused by the kernel): at most one chain workgroup
-  // per CU.  Batches of at most one wave per CU run one wave per workgroup
-  // (one SIMD per CU busy, every CU used); larger ones run four waves per
-  // workgroup, one per SIMD.
-  const int threads = (int64_t)n <= (int64_t)device_cu_count() * kWave ? kWave : 4 * kWave;
-  const dim3 grid((unsigned)ceil_div(n, threads)), block(threads);
-  const size_t lds = chain_lds_reserve();
-  switch (mode) {
-    case KVGOV_NONE: hipLaunchKernelGGL(k_chains<KVGOV_NONE>, grid, block, lds, s, a); break;
-    case KVGOV_ROOT: hipLaunchKernelGGL(k_chains<KVGOV_ROOT>, grid, block, lds, s, a); break;
-    default: hipLaunchKernelGGL(k_chains<KVGOV_BOUNDARY>, grid, block, lds, s, a); break;
+  // then takes nearly every issue slot, so the workgroups reserve LDS (unused
+  // beyond the kernel's own) to bound how many share a CU.
+  const int slots = pair_slots(n);
+  if (slots) {
+    // wave pairs (rounds wave + schedule wave), one or two pairs per CU
+    constexpr int P = KVGOV_PAIRS;
+    const dim3 grid((unsigned)ceil_div(n, kWave * P)), block(2 * P * kWave);
+    const size_t lds = pair_lds_reserve(slots);
+    switch (mode) {
+      case KVGOV_NONE: hipLaunchKernelGGL((k_chains_pair<KVGOV_NONE, P>), grid, block, lds, s, a); break;
+      case KVGOV_ROOT: hipLaunchKernelGGL((k_chains_pair<KVGOV_ROOT, P>), grid, block, lds, s, a); break;
+      default: hipLaunchKernelGGL((k_chains_pair<KVGOV_BOUNDARY, P>), grid, block, lds, s, a); break;
+    }
+  } else {
+    // at most one workgroup per CU; batches of at most one wave per CU run
+    // one wave per workgroup, larger ones four (one per SIMD)
+    const int threads = (int64_t)n <= (int64_t)device_cu_count() * kWave ? kWave : 4 * kWave;
+    const dim3 grid((unsigned)ceil_div(n, threads)), block(threads);
+    const size_t lds = chain_lds_reserve();
+    switch (mode) {
+      case KVGOV_NONE: hipLaunchKernelGGL(k_chains<KVGOV_NONE>, grid, block, lds, s, a); break;
+      case KVGOV_ROOT: hipLaunchKernelGGL(k_chains<KVGOV_ROOT>, grid, block, lds, s, a); break;
+      default: hipLaunchKernelGGL(k_chains<KVGOV_BOUNDARY>, grid, block, lds, s, a); break;
+    }
   }
   int rc = launch_status();
   if (scratch && hipFreeAsync(scratch, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;

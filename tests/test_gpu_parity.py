@@ -354,3 +354,20 @@ def test_tiny_workload_end_to_end():
         hits = c.lookup(hl, dev(wl.lookup.blk_offsets())).cpu().numpy()
     assert np.array_equal(hits, T.lookup(wlk, wl.lookup.blk_offsets()))
     assert np.array_equal(hits, wl.lookup.expect_hits[W.ROOT])
+
+
+@pytest.mark.parametrize("n_req", [20000, 30000])
+def test_chains_between_one_and_two_pairs_per_cu(n_req):
+    """Batch sizes where the wave-pair kernel runs two pairs per CU
+    (between 64 and 128 requests per CU on a 256-CU device)."""
+    g = np.random.default_rng(n_req)
+    lens = g.integers(0, 300, n_req)
+    b = ragged(n_req, lens, P=11)
+    Kb, ids = secret(12, 11)
+    sd = K.salts(Kb, dev(ids))
+    osalts = O.salts(Kb, ids)
+    for mode in (W.NONE, W.ROOT, W.BOUNDARY):
+        got = gpu_chains(b, sd, mode).cpu().numpy()
+        want = O.hash_chains_parallel(b.tokens, b.tok_offsets, b.principal, osalts, mode,
+                                      b.boundary_tok)
+        assert np.array_equal(got, want), mode
