@@ -79,6 +79,42 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# Kernel sources whose hash identifies the build a traffic record was taken on.
+KERNEL_SOURCES = {
+    "chains": ["chains.hip", "sha256_cdna4.h", "common.h"],
+    "cache": ["cache.hip", "common.h"],
+}
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "hbm_traffic.md")
+
+
+def sources_sha256(group: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[group]:
+        with open(os.path.join(ROOT, "paper_2608_09225_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(kernel: str, workload: str, group: str):
+    """HBM bytes per launch (fetch + write, scaled by a copy kernel) from the
+    committed counter record, or None if the kernel's sources changed since."""
+    try:
+        with open(TRAFFIC_RECORD) as f:
+            rows = [l for l in f if l.startswith("| `")]
+    except OSError:
+        return None
+    want = sources_sha256(group)
+    for row in rows:
+        cells = [c.strip().strip("`") for c in row.strip().strip("|").split("|")]
+        if len(cells) >= 5 and cells[0] == kernel and cells[1] == workload:
+            if cells[2] != want:
+                return None
+            return {"fetch_bytes": int(cells[3]), "write_bytes": int(cells[4]),
+                    "bytes": int(cells[3]) + int(cells[4])}
+    return None
+
+
 def compressions(batch: W.Batch, mode: int) -> int:
     """Compressions the definition needs: 2 per full block, plus one for the
     128-byte boundary block (boundary mode, 0 < k < n_full)."""
@@ -354,10 +390,14 @@ def main():
     look_bytes = {m: lookup_bytes(B, got_hits[m]) for m in modes}
     look_mean = {m: float(np.mean(ts)) for m, ts in look_t.items()}
     look_gbs = float(np.mean([look_bytes[m] / look_mean[m] for m in modes])) / 1e9
+    g_look = 1  # lanes per request the library picks for this batch size
+    while g_look < 64 and B.n * g_look * 2 <= (1 << 18):
+        g_look <<= 1
+    ltr = recorded_traffic(f"k_lookup<{g_look}>", wl.name, "cache")
     roof_lookup = {
         "bound": "hbm", "kernel": "k_lookup (first-miss prefix lookup)",
         "achieved": look_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-        "frac": look_gbs / HBM_PEAK_GBS, "traffic": None,
+        "frac": look_gbs / HBM_PEAK_GBS, "traffic": None if ltr is None else ltr["bytes"],
         "bytes_per_launch": {W.MODE_NAMES[m]: b for m, b in look_bytes.items()},
         "launch_ms": {W.MODE_NAMES[m]: t * 1e3 for m, t in look_mean.items()},
         "examined_blocks_per_launch": {
@@ -392,11 +432,23 @@ def main():
             spans.append((max(ends) - min(starts)) * 1e-3)
         concurrent = sum(ops.values()) / float(np.mean(spans)) / 1e12
         waves = int(np.ceil(X.n / 64))
+        cus = torch.cuda.get_device_properties(dev).multi_processor_count
+        pair = X.n <= 2 * 64 * cus
+        kname = "k_chains_pair" if pair else "k_chains"
+        targs = (lambda m: f"<{m},1>") if pair else (lambda m: f"<{m}>")
+        tr = {m: recorded_traffic(f"{kname}{targs(m)}", wl.name, "chains") for m in modes}
+        traffic = None
+        if all(t is not None for t in tr.values()):
+            traffic = float(np.mean([t["bytes"] for t in tr.values()]))
         result["roofline"] = {
-            "bound": "alu", "kernel": "k_chains (chained block hashing)",
+            "bound": "alu", "kernel": f"{kname} (chained block hashing)",
             "achieved": achieved, "peak": INT_PEAK_TOPS,
             "unit": "Tops/s (32-bit integer vector ops)", "frac": achieved / INT_PEAK_TOPS,
-            "traffic": None,
+            "traffic": traffic,
+            "traffic_note": "HBM bytes per launch, FETCH_SIZE + WRITE_SIZE scaled by a 1 GiB "
+                            "copy kernel (profiles/hbm_traffic.md); null if the kernel "
+                            "sources changed since",
+            "algorithmic_bytes_per_launch": 64 * nX + 32 * nX,
             "ops_per_compression": OPS_PER_COMPRESSION,
             "ops_per_compression_2input": OPS_PER_COMPRESSION_2INPUT,
             "ops_per_launch": {W.MODE_NAMES[m]: o for m, o in ops.items()},

@@ -971,7 +971,9 @@ int kvgov_block_offsets(const int64_t *tok_offsets, int32_t n, int32_t block_siz
 
 // Longest-first ordering pays once the batch has about as many waves as the
 // chip has SIMDs; below that every wave has a SIMD of its own from the start
-// and the kernel takes as long as its longest chain in any order.
+// and the kernel takes as long as its longest chain in any order.  (Batches
+// that run on the wave-pair kernel are resident all at once and are never
+// ordered.)
 static int64_t order_min_requests() { return (int64_t)device_cu_count() * 4 * kWave / 2; }
 
 int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_offsets,
@@ -1006,8 +1008,9 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
   a.status = status;
   a.order = nullptr;
 
+  const int slots = pair_slots(n);
   int32_t *scratch = nullptr;
-  if (n >= order_min_requests()) {
+  if (!slots && n >= order_min_requests()) {
     const size_t bytes = sizeof(int32_t) * ((size_t)kOrderBuckets + (size_t)n);
     if (hipMallocAsync(reinterpret_cast<void **>(&scratch), bytes, s) != hipSuccess)
       return KVGOV_E_NOMEM;
@@ -1027,7 +1030,6 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
   // the waves of concurrent launches on the same SIMDs, and the older wave
   // then takes nearly every issue slot, so the workgroups reserve LDS (unused
   // beyond the kernel's own) to bound how many share a CU.
-  const int slots = pair_slots(n);
   if (slots) {
     // wave pairs (rounds wave + schedule wave), one or two pairs per CU
     constexpr int P = KVGOV_PAIRS;
