@@ -17,6 +17,15 @@ reported beside it.  The roofline entry is for the chain-hashing kernel,
 the dominant kernel of the step, timed with HIP events on its own stream;
 the lookup kernel's HBM roofline is reported beside it.
 
+Beside the bench line's own fields: per-phase rates for every mode (median,
+mean and min launch times of salts, chains, clear, insert, lookup, with
+tokens/s, block hashes/s, compressions/s, insert keys/s, lookups/s and block
+probes/s), the insert kernel's HBM roofline, the critical-path ceiling (the
+longest request hashed alone), the device's measured peaks (integer-VALU and
+32-byte random-gather microbenchmarks, a 1 GiB copy) with the fractions of
+those, and the CPU oracle per phase, on one core and with the host's CPU
+model and SHA extension flag.
+
 --config {tiny,template,large} runs the same kind of step on those
 workloads (large: chains + insert + a re-lookup of the inserted batch);
 --config probe times lookups alone against the 8M-key resident table (the
@@ -60,6 +69,10 @@ OPS_PER_COMPRESSION_2INPUT = 1672
 # request two 8-byte offsets and a 4-byte result.
 LOOKUP_BYTES_PER_BLOCK = 64
 LOOKUP_BYTES_PER_REQUEST = 20
+# Insert: a new key reads its 32-byte query and one slot, and writes the slot;
+# a key already present reads the query and the slot holding it.
+INSERT_BYTES_NEW = 96
+INSERT_BYTES_PRESENT = 64
 
 DESCRIPTIONS = {
     "paper": "paper-shaped shared prefix: 4096 requests x 2 batches (insert, re-lookup with "
@@ -146,42 +159,97 @@ def capped(b: W.Batch, max_blocks: int) -> W.Batch:
     return b if n >= b.n else b.subset(np.arange(max(n, 1)))
 
 
+def host_cpu_info() -> dict:
+    info = {"os_cpu_count": os.cpu_count(), "model": None, "sha_ni": None}
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name") and info["model"] is None:
+                    info["model"] = line.split(":", 1)[1].strip()
+                if line.startswith("flags") and info["sha_ni"] is None:
+                    info["sha_ni"] = "sha_ni" in line.split(":", 1)[1].split()
+    except OSError:
+        pass
+    return info
+
+
+def cpu_salt_cost(wl: W.Workload, min_seconds: float = 0.2) -> float:
+    """Seconds per HMAC key derivation with the oracle (one process)."""
+    import oracle as O
+    n, t0 = 0, time.perf_counter()
+    while True:
+        O.salts(wl.K, wl.principal_ids)
+        n += wl.P
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            return dt / n
+
+
 def cpu_baseline(wl: W.Workload, processes: int, max_blocks: int):
     """The oracle, untouched, running the same step on the host cores (on the
     first requests of each batch when the workload is larger than
-    ``max_blocks`` blocks per batch)."""
+    ``max_blocks`` blocks per batch), each phase timed on its own; plus the
+    chains of a few requests on one core and the per-key HMAC cost."""
     import oracle as O
     if wl.name == "probe":
         return cpu_baseline_probe(wl, processes)
     same = wl.name == "large"
     A = capped(wl.insert, max_blocks)
     B = A if same else capped(wl.lookup, max_blocks)
-    t0 = time.perf_counter()
+    clock = time.perf_counter
+    t = {"salts": 0.0, "chains": 0.0, "insert": 0.0, "lookup": 0.0}
+    t0 = clock()
     salts = O.salts(wl.K, wl.principal_ids)
-    tokens = 0
-    lookups = 0
+    t["salts"] = clock() - t0
+    tokens = keys = lookups = 0
     for mode in wl.modes:
         hashes = {}
         for name, b in (("insert", A), ("lookup", B)):
             if name == "lookup" and same:
                 hashes[name] = hashes["insert"]
                 continue
+            t0 = clock()
             hashes[name] = O.hash_chains_parallel(b.tokens, b.tok_offsets, b.principal, salts,
                                                   mode, b.boundary_tok, processes=processes)
+            t["chains"] += clock() - t0
             tokens += 16 * int(b.block_counts().sum())
         T = O.Table()
+        t0 = clock()
         T.insert(hashes["insert"], A.blk_offsets())
+        t["insert"] += clock() - t0
+        keys += hashes["insert"].shape[0]
+        t0 = clock()
         T.lookup(hashes["lookup"], B.blk_offsets())
+        t["lookup"] += clock() - t0
         lookups += B.n
-    dt = time.perf_counter() - t0
+    dt = sum(t.values())
+    # one core: the chains of the first requests of the insert batch
+    one = capped(A, 20000)
+    t0 = clock()
+    O.hash_chains(one.tokens, one.tok_offsets, one.principal, salts, wl.modes[0],
+                  one.boundary_tok)
+    t1 = clock() - t0
     whole = A is wl.insert and (same or B is wl.lookup)
     what = "one full step of the same workload" if whole else \
         f"the step on the first {A.n} (insert) / {B.n} (lookup) requests"
     return {"value": tokens / dt, "unit": "tokens/s", "cores": processes, "kind": "oracle",
             "sample": (f"{what} ({tokens} block tokens hashed, {lookups} lookups, "
                        f"{len(wl.modes)} mode(s)) in {dt:.1f} s; chains over {processes} "
-                       "worker processes, table in one process"),
-            "seconds": dt, "lookups_per_s": lookups / dt}
+                       "worker processes, salts and table in one process"),
+            "seconds": dt, "lookups_per_s": lookups / dt,
+            "phases": {
+                "salts_us_per_key": t["salts"] / wl.P * 1e6,
+                "chains_tokens_per_s": tokens / t["chains"],
+                "insert_keys_per_s": keys / t["insert"],
+                "lookup_lookups_per_s": lookups / t["lookup"],
+            },
+            "single_core": {
+                "chains_tokens_per_s": 16 * int(one.block_counts().sum()) / t1,
+                "sample": f"chains of the first {one.n} insert requests, "
+                          f"{W.MODE_NAMES[wl.modes[0]]} mode",
+                "salts_us_per_key": cpu_salt_cost(wl) * 1e6,
+            },
+            "host": host_cpu_info()}
 
 
 def cpu_baseline_probe(wl: W.Workload, processes: int, resident: int = 20000):
@@ -205,7 +273,50 @@ def cpu_baseline_probe(wl: W.Workload, processes: int, resident: int = 20000):
             "sample": (f"lookup of the {Pb.n} probes copied from the first {resident} resident "
                        f"requests, against their {hr.shape[0]} keys, in {dt:.1f} s "
                        "(one process; hashing not timed)"),
-            "seconds": dt}
+            "seconds": dt, "host": host_cpu_info()}
+
+
+def measured_peaks(dev, slots: int = 1 << 24) -> dict:
+    """What the device reaches on the microbenchmarks of libkvgov_peaks (the
+    best of five launches each) and on a 1 GiB device-to-device copy."""
+    import torch
+    from paper_2608_09225_amd import peaks as P
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    s = torch.cuda.Stream(device=dev)
+    out = torch.empty(cus * 32 * P.THREADS, dtype=torch.int32, device=dev)
+    table = torch.zeros((slots, 32), dtype=torch.uint8, device=dev)
+    src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+
+    def best(launch):
+        rates = []
+        for i in range(6):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(s)
+            work = launch()
+            e1.record(s)
+            e1.synchronize()
+            if i:
+                rates.append(work / (e0.elapsed_time(e1) * 1e-3))
+        return max(rates)
+
+    torch.cuda.synchronize()
+    valu = best(lambda: P.valu(out, cus * 8, 4096, stream=s))
+    gather = best(lambda: P.gather(table, out, cus * 32, 16, stream=s))
+
+    def copy():
+        with torch.cuda.stream(s):
+            dst.copy_(src)
+        return 2 * src.numel()
+    cp = best(copy)
+    torch.cuda.synchronize()
+    del table, src, dst
+    return {"int_valu_tops": valu / 1e12, "gather32_gbs": gather / 1e9,
+            "gather32_table_bytes": slots * 32, "copy_gbs": cp / 1e9,
+            "note": "best of 5 launches: independent rotate/add3/xor3 chains, 8 waves per "
+                    "SIMD; 32-byte reads at random slots of a table; a 1 GiB copy (read + "
+                    "write bytes)"}
 
 
 def main():
@@ -268,7 +379,7 @@ def main():
     caches = {m: K.Cache(wl.log2_slots) for m in modes}
     main_s = torch.cuda.current_stream()
     streams = {m: torch.cuda.Stream(device=dev) for m in modes}  # default priority
-    ev_chain, ev_look = [], []
+    ev_chain, ev_look, ev_salts, ev_clear, ev_ins = [], [], [], [], []
 
     def bview(m):
         return out[m][0:nA], (out[m][0:nA] if relookup_same else out[m][nA:])
@@ -289,9 +400,23 @@ def main():
         probe_hash_ms = e0.elapsed_time(e1)
         log(f"set-up: {nX} blocks hashed in {probe_hash_ms:.2f} ms, {n_new} keys resident")
 
+    def timed(evs, key, s):
+        """Records a start event now on ``s``; returns a closure recording the end."""
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+
+        def end():
+            e1.record(s)
+            evs.append((key, e0, e1))
+        return end
+
     def step(record: bool):
         if not probe_only:
+            end = timed(ev_salts, None, main_s) if record else None
             K.salts(wl.K, ids, out=salts, stream=main_s)
+            if end:
+                end()
         salted = torch.cuda.Event()
         salted.record(main_s)
         done = []
@@ -300,7 +425,10 @@ def main():
             s.wait_event(salted)
             hA, hB = bview(m)
             if not probe_only:
+                end = timed(ev_clear, m, s) if record else None
                 caches[m].clear(stream=s)
+                if end:
+                    end()
                 if record:
                     e0 = torch.cuda.Event(enable_timing=True)
                     e1 = torch.cuda.Event(enable_timing=True)
@@ -311,7 +439,10 @@ def main():
                 if record:
                     e1.record(s)
                     ev_chain.append((m, e0, e1))
+                end = timed(ev_ins, m, s) if record else None
                 caches[m].insert(hA, boA, sync=False, stream=s)
+                if end:
+                    end()
             if record:
                 l0 = torch.cuda.Event(enable_timing=True)
                 l1 = torch.cuda.Event(enable_timing=True)
@@ -431,12 +562,12 @@ def main():
             ends = [ref.elapsed_time(e1) for _, _, e1 in grp]
             spans.append((max(ends) - min(starts)) * 1e-3)
         concurrent = sum(ops.values()) / float(np.mean(spans)) / 1e12
-        waves = int(np.ceil(X.n / 64))
+        waves = int(np.ceil(X.n / 64))  # one lane per request
         cus = torch.cuda.get_device_properties(dev).multi_processor_count
-        pair = X.n <= 2 * 64 * cus
-        kname = "k_chains_pair" if pair else "k_chains"
-        targs = (lambda m: f"<{m},1>") if pair else (lambda m: f"<{m}>")
-        tr = {m: recorded_traffic(f"{kname}{targs(m)}", wl.name, "chains") for m in modes}
+        # the library's launch policy: the lane-pair kernel while the batch
+        # fits in two 64-request workgroups per CU
+        kname = "k_chains_lp" if X.n <= 2 * 64 * cus else "k_chains"
+        tr = {m: recorded_traffic(f"{kname}<{m}>", wl.name, "chains") for m in modes}
         traffic = None
         if all(t is not None for t in tr.values()):
             traffic = float(np.mean([t["bytes"] for t in tr.values()]))
@@ -457,6 +588,9 @@ def main():
             "launch_requests": X.n,
             "longest_chain_blocks": int(X.block_counts().max()),
             "parallelism_ceiling": min(1.0, waves / (CUS * SIMDS_PER_CU)),
+            "parallelism_ceiling_note": "ceil(requests / 64) / 1024 SIMDs: waves at one lane "
+                                        "per request (the lane-pair kernel runs three waves "
+                                        "per 64 requests)",
             "concurrent_modes_achieved": concurrent,
             "concurrent_modes_frac": concurrent / INT_PEAK_TOPS,
         }
@@ -468,6 +602,99 @@ def main():
             result["retention_boundary_vs_none"] = s["boundary"] / max(1, s["none"])
             result["retention_root_vs_none"] = s["root"] / max(1, s["none"])
     result["keys_in_table"] = n_keys
+
+    # ---- per-phase rates (HIP events on each call's own stream) ----------
+    def stats(ts):
+        a = np.asarray(ts) * 1e3
+        return {"ms_mean": float(a.mean()), "ms_median": float(np.median(a)),
+                "ms_min": float(a.min())}
+
+    phases = {}
+    if ev_salts:
+        st = stats(per(ev_salts)[None])
+        phases["salts"] = {**st, "salts_per_s": wl.P / (st["ms_median"] * 1e-3)}
+    clear_t, ins_t = per(ev_clear), per(ev_ins)
+    for m in modes:
+        ph = {}
+        if not probe_only:
+            st = stats(chain_t[m])
+            sec = st["ms_median"] * 1e-3
+            ph["chains"] = {**st, "blocks": nX, "tokens_per_s": 16 * nX / sec,
+                            "block_hashes_per_s": nX / sec,
+                            "compressions_per_s": compressions(X, m) / sec}
+            ph["clear"] = stats(clear_t[m])
+            st = stats(ins_t[m])
+            sec = st["ms_median"] * 1e-3
+            n_new = n_keys[W.MODE_NAMES[m]]
+            ibytes = INSERT_BYTES_NEW * n_new + INSERT_BYTES_PRESENT * (nA - n_new)
+            ph["insert"] = {**st, "keys": nA, "new_keys": n_new, "keys_per_s": nA / sec,
+                            "algorithmic_bytes": ibytes, "gbs": ibytes / sec / 1e9}
+        st = stats(look_t[m])
+        sec = st["ms_median"] * 1e-3
+        ex = roof_lookup["examined_blocks_per_launch"][W.MODE_NAMES[m]]
+        ph["lookup"] = {**st, "lookups_per_s": B.n / sec, "block_probes_per_s": ex / sec}
+        phases[W.MODE_NAMES[m]] = ph
+    result["phases"] = phases
+
+    if not probe_only:
+        ins_gbs = float(np.mean([phases[W.MODE_NAMES[m]]["insert"]["gbs"] for m in modes]))
+        itr = recorded_traffic("k_insert", wl.name, "cache")
+        result["roofline_insert"] = {
+            "bound": "hbm", "kernel": "k_insert (set-union insert)", "achieved": ins_gbs,
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ins_gbs / HBM_PEAK_GBS,
+            "traffic": None if itr is None else itr["bytes"],
+            "bytes_note": f"{INSERT_BYTES_NEW} B per new key (query read, slot read, slot "
+                          f"write), {INSERT_BYTES_PRESENT} B per present key",
+        }
+        # Critical path: the per-block latency of the lane-pair kernel under a
+        # realistic load (the longest request replicated into one 64-request
+        # workgroup per CU; a single workgroup on an otherwise idle GPU runs
+        # at a lower clock), times the longest chain.
+        r = int(np.argmax(X.block_counts()))
+        one = X.subset(np.array([r]))
+        nrep = 64 * cus
+        L1 = int(one.tok_offsets[-1])
+        rep = W.Batch(np.tile(one.tokens, nrep), np.arange(nrep + 1, dtype=np.int64) * L1,
+                      np.repeat(one.principal, nrep), np.repeat(one.boundary_tok, nrep))
+        o = dict(tokens=to(rep.tokens), tok_offsets=to(rep.tok_offsets),
+                 principal=to(rep.principal), boundary_tok=to(rep.boundary_tok),
+                 blk_offsets=to(rep.blk_offsets()))
+        oh = torch.empty((int(rep.block_counts().sum()), 32), dtype=torch.uint8, device=dev)
+        m0 = modes[0]
+        ts = []
+        for i in range(4):
+            end = timed(ts, None, main_s)
+            K.hash_chains(o["tokens"], o["tok_offsets"], o["principal"], salts, m0,
+                          o["boundary_tok"], blk_offsets=o["blk_offsets"], out=oh,
+                          status=status, check=False, stream=main_s)
+            end()
+        torch.cuda.synchronize()
+        K.check_status(status, "critical-path launch")
+        ok_rep = bool(np.array_equal(oh[:int(one.block_counts()[0])].cpu().numpy(),
+                                     out[m0][int(bo[r]):int(bo[r + 1])].cpu().numpy()))
+        gates["G1_bitexact_sampled"] = bool(gates["G1_bitexact_sampled"] and ok_rep)
+        t_crit = min(e0.elapsed_time(e1) for _, e0, e1 in ts[1:]) * 1e-3
+        ideal = ops[m0] / (INT_PEAK_TOPS * 1e12)
+        roof = result["roofline"]
+        roof["critical_path_ms"] = t_crit * 1e3
+        roof["us_per_block_on_critical_path"] = t_crit / one.block_counts()[0] * 1e6
+        roof["critical_path_ceiling"] = min(1.0, ideal / t_crit)
+        roof["critical_path_note"] = (f"the longest request ({int(one.block_counts()[0])} blocks) "
+                                      f"replicated {nrep} times, one launch; ceiling = "
+                                      "(launch ops at peak) / its duration")
+        del o, oh
+
+    log("measuring device peaks (microbenchmarks)")
+    mp = measured_peaks(dev)
+    result["measured_peaks"] = mp
+    roof = result["roofline"]
+    if roof["bound"] == "alu":
+        roof["frac_of_measured_peak"] = roof["achieved"] / mp["int_valu_tops"]
+    for key in ("roofline_lookup", "roofline_insert", "roofline"):
+        rr = result.get(key)
+        if rr and rr["bound"] == "hbm":
+            rr["frac_of_measured_gather32"] = rr["achieved"] / mp["gather32_gbs"]
+
     h = args.steps // 2
     a1, a2 = np.mean(per_step[:h]), np.mean(per_step[h:])
     gates["G3_two_halves_within_5pct"] = bool(abs(a1 - a2) / max(a1, a2) < 0.05)

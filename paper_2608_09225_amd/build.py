@@ -1,4 +1,6 @@
-"""Builds libkvgov.so in-tree with hipcc for gfx950."""
+"""Builds the in-tree shared libraries with hipcc for gfx950:
+libkvgov.so (the hashing / cache path) and libkvgov_peaks.so (measured-peak
+microbenchmarks used by the measurement harness)."""
 from __future__ import annotations
 
 import os
@@ -7,7 +9,10 @@ import subprocess
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-SOURCES = ["csrc/chains.hip", "csrc/cache.hip"]
+LIBS = {
+    "libkvgov.so": ["csrc/chains.hip", "csrc/cache.hip"],
+    "libkvgov_peaks.so": ["csrc/peaks.hip"],
+}
 OUT = os.path.join(HERE, "libkvgov.so")
 ARCH = "gfx950"
 
@@ -30,9 +35,10 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False) -> str:
-    tmp = OUT + ".tmp"
-    cmd = [hipcc(), *FLAGS, "-o", tmp, *[os.path.join(HERE, s) for s in SOURCES]]
+def build_one(name: str, sources, verbose: bool = False) -> str:
+    out = os.path.join(HERE, name)
+    tmp = out + ".tmp"
+    cmd = [hipcc(), *FLAGS, "-o", tmp, *[os.path.join(HERE, s) for s in sources]]
     res = subprocess.run(cmd, capture_output=True, text=True)
     noise = "'-packed-fp32-ops' is not a recognized feature"
     msgs = "\n".join(l for l in (res.stdout + res.stderr).splitlines() if noise not in l)
@@ -40,7 +46,14 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{' '.join(cmd)}\n{msgs}")
     if verbose and msgs.strip():
         print(msgs, file=sys.stderr)
-    os.replace(tmp, OUT)
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    """Builds every library; returns the path of libkvgov.so."""
+    for name, sources in LIBS.items():
+        build_one(name, sources, verbose)
     return OUT
 
 

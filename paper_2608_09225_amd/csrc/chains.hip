@@ -5,10 +5,14 @@
 // root (Sec. 4.1) or at the divergence boundary k (Sec. 4.2).
 //
 // Execution model.  A chain is a strict sequence of SHA-256 compressions
-// (h_j needs h_{j-1}), so one lane owns one request and walks its chain; a
-// wave therefore advances 64 chains at once, and all parallelism comes from
-// the batch.  Requests are ordered longest first (LPT) so that the 64 lanes
-// of a wave carry similar block counts and long chains start early.
+// (h_j needs h_{j-1}), so all parallelism comes from the batch.  Two kernels:
+//   * k_chains: one lane owns one request and walks its chain (a wave
+//     advances 64 chains); for batches that fill every SIMD, ordered longest
+//     first (LPT) so that the lanes of a wave carry similar block counts and
+//     long chains start early;
+//   * k_chains_lp: three waves per 64 requests, two lanes per request for
+//     the rounds and a third wave for the message schedule, which shortens
+//     every chain; for batches of at most two workgroups per CU.
 //
 // Per block a lane issues two compressions: (IV; h_{j-1} || T_j[0..7]) and
 // (state; T_j[8..15] || padding of a 96-byte message).  Three cases leave
@@ -37,11 +41,8 @@
 #include "common.h"
 #include "sha256_cdna4.h"
 
-#ifndef KVGOV_PAIR_DEFAULT
-#define KVGOV_PAIR_DEFAULT 1
-#endif
-#ifndef KVGOV_PAIRS
-#define KVGOV_PAIRS 1
+#ifndef KVGOV_LANE_PAIR
+#define KVGOV_LANE_PAIR 1  // 0: the single-wave kernel for every batch
 #endif
 
 namespace kvgov {
@@ -58,6 +59,24 @@ __device__ __forceinline__ void load_raw(const int32_t *p, u32x4 raw[4]) {
   const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
 #pragma unroll
   for (int i = 0; i < 4; ++i) raw[i] = q[i];
+}
+
+// Token prefetch.  T <- the block held in raw (block j), then raw <- block
+// j + 1 (block j again when j is the last, so that the load is
+// unconditional).  The scheduling barriers pin the load right after the last
+// read of raw: it then writes raw's registers in place, and its latency hides
+// behind a block's compressions.  (Issued before those reads, or under a
+// condition, the load lands in temporaries that are copied into raw at once,
+// which waits for it.)  Callers take the next block before storing the
+// current digest: a wait for the load must not also wait for a store issued
+// after it.
+__device__ __forceinline__ void swap_block(const u32x4 raw[4], uint32_t T[16]);
+__device__ __forceinline__ void take_block(u32x4 raw[4], uint32_t T[16], const int32_t *tp,
+                                           int64_t j, int64_t nf) {
+  swap_block(raw, T);
+  __builtin_amdgcn_sched_barrier(0);
+  load_raw(tp + 16 * (j + 1 < nf ? j + 1 : j), raw);
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 __device__ __forceinline__ void swap_block(const u32x4 raw[4], uint32_t T[16]) {
@@ -482,14 +501,12 @@ __global__ __launch_bounds__(256) void k_chains(ChainArgs a) {
   for (int w = 0; w < 8; ++w) H[w] = q.salted_root ? q.sig[w] : 0u;
 
   u32x4 nxt[4];
+  uint32_t T[16];  // tokens of block j
   load_raw(q.tp, nxt);
+  take_block(nxt, T, q.tp, 0, nf);
   const bool plain_first = !q.salted_root;
 
   for (int64_t j = 0; j < nf; ++j) {
-    uint32_t T[16];
-    swap_block(nxt, T);
-    if (j + 1 < nf) load_raw(q.tp + 16 * (j + 1), nxt);
-
     const bool u0 = plain_first && j == 0;
     const bool bnd = (MODE == KVGOV_BOUNDARY) && j == q.k && q.k > 0;
     if (MODE == KVGOV_ROOT || !__any(u0 || bnd)) {
@@ -508,139 +525,242 @@ __global__ __launch_bounds__(256) void k_chains(ChainArgs a) {
     } else {
       special_block(H, T, q.sig, u0, bnd);
     }
+    // the next block's tokens before the digest store (see take_block)
+    take_block(nxt, T, q.tp, j + 1 < nf ? j + 1 : j, nf);
     store_digest(q.out + j * 32, H);
   }
 }
 
 // ---------------------------------------------------------------------------
-// wave-pair chain kernel
+// helpers of the lane-pair kernel
 // ---------------------------------------------------------------------------
-//
-// A chain is latency-bound: one wave advances 64 chains at the issue rate of
-// its SIMD, and a block costs ~2800 vector instructions, a third of them the
-// message schedule.  The schedule does not feed back into the rounds except
-// through its output words, so a second wave on another SIMD computes it and
-// hands the words over through LDS:
-//   wave 0 ("rounds")   : the 64 rounds of each compression, state in registers;
-//   wave 1 ("schedule") : W[16..63] of both compressions of every block.
-// Lane l of both waves owns the same request.  Per block j:
-//   phase 1  rounds: C1 rounds 0-15 (message h_{j-1} || T[0..7] in registers)
-//            schedule: reads h_{j-1} from LDS, computes C1's W[16..31]
-//   phase 2  rounds: C1 rounds 16-31       schedule: C1's W[32..47]
-//   phase 3  rounds: C1 rounds 32-47       schedule: C1's W[48..63]
-//   phase 4  rounds: C1 rounds 48-63, then all of C2 (its W[16..63] were
-//            computed during block j-1: the C2 message T[8..15] || padding
-//            depends on tokens only); writes h_j to LDS and the digest
-//            schedule: C2's W[16..63] of block j+1 (double buffered)
-// with a workgroup barrier after each phase.  Iterations where a lane of the
-// wave has a special block (unsalted first block, boundary block) run the
-// special path entirely on the rounds wave; the schedule wave then only
-// prepares the next block's C2 words.  Both waves derive every branch and
-// trip count from the same per-lane data, so they meet the same barriers.
 
-struct PairLds {
-  uint32_t h[8][kWave];          // h_{j-1} per lane
-  uint32_t w1[48][kWave];        // C1's W[16..63]
-  uint32_t w2[2][48][kWave];     // C2's W[16..63], double buffered by block parity
-};
-
-struct Sha8 {
-  uint32_t a, b, c, d, e, f, g, h;
-};
-
-__device__ __forceinline__ void round_w(Sha8 &s, uint32_t kt, uint32_t w) {
-  const uint32_t t1 = s.h + big_sigma1(s.e) + ch(s.e, s.f, s.g) + kt + w;
-  const uint32_t t2 = big_sigma0(s.a) + maj(s.a, s.b, s.c);
-  s.h = s.g; s.g = s.f; s.f = s.e; s.e = s.d + t1;
-  s.d = s.c; s.c = s.b; s.b = s.a; s.a = t1 + t2;
-}
-
-__device__ __forceinline__ Sha8 sha8_iv() {
-  return Sha8{kSha.H0[0], kSha.H0[1], kSha.H0[2], kSha.H0[3],
-              kSha.H0[4], kSha.H0[5], kSha.H0[6], kSha.H0[7]};
-}
-
-__device__ __forceinline__ Sha8 sha8_load(const uint32_t st[8]) {
-  return Sha8{st[0], st[1], st[2], st[3], st[4], st[5], st[6], st[7]};
-}
-
-__device__ __forceinline__ void sha8_add(uint32_t st[8], const Sha8 &s) {
-  st[0] += s.a; st[1] += s.b; st[2] += s.c; st[3] += s.d;
-  st[4] += s.e; st[5] += s.f; st[6] += s.g; st[7] += s.h;
-}
-
-// 16 schedule words from LDS into registers
-__device__ __forceinline__ void load16(uint32_t w[16], const uint32_t (*wl)[kWave], int base,
-                                       int lane) {
-#pragma unroll
-  for (int i = 0; i < 16; ++i) w[i] = wl[base + i][lane];
-}
-
-// rounds t0..t0+11 and t0..t0+3 with W[t0 + i] = w[i]
-__device__ __forceinline__ void rounds12(Sha8 &s, const uint32_t *w, int t0) {
-#pragma unroll
-  for (int i = 0; i < 12; ++i) round_w(s, kSha.K[t0 + i], w[i]);
-}
-__device__ __forceinline__ void rounds4(Sha8 &s, const uint32_t *w, int t0) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) round_w(s, kSha.K[t0 + i], w[i]);
-}
-
-// 16 schedule words W[t..t+15] from the rolling window w (W[t-16..t-1]),
-// stored to out[base + i][lane]
-__device__ __forceinline__ void sched16(uint32_t w[16], uint32_t (*out)[kWave], int base,
-                                        int lane) {
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    w[i] = small_sigma1(w[(i + 14) & 15]) + w[(i + 9) & 15] + small_sigma0(w[(i + 1) & 15]) +
-           w[i];
-    out[base + i][lane] = w[i];
-  }
-}
-
-// Block-count summary of a request used to keep the waves of a workgroup in
-// lockstep: every wave evaluates it for every pair's request of its lane.
-struct PairPeek {
+// Block-count summary of a request, used to keep the waves of a workgroup in
+// lockstep: every wave decides trip counts and special iterations over all
+// requests of the workgroup.
+struct ReqPeek {
   int64_t nf;
   int64_t k;
   bool plain_first;
 };
 
 template <int MODE>
-__device__ __forceinline__ PairPeek pair_peek(const ChainArgs &a, int32_t i) {
-  PairPeek p{0, -1, false};
+__device__ __forceinline__ ReqPeek req_peek(const ChainArgs &a, int32_t i) {
+  ReqPeek p{0, -1, false};
   if (i < a.n) {
     ChainReq q;
     const int32_t r = a.order ? a.order[i] : i;
-    if (chain_setup<MODE>(a, r, q)) p = PairPeek{q.nf, q.k, !q.salted_root};
+    if (chain_setup<MODE>(a, r, q)) p = ReqPeek{q.nf, q.k, !q.salted_root};
   }
   return p;
 }
 
 template <int MODE>
-__device__ __forceinline__ bool pair_special(const PairPeek &p, int64_t j) {
+__device__ __forceinline__ bool req_special(const ReqPeek &p, int64_t j) {
   const bool act = j < p.nf;
   return act && ((p.plain_first && j == 0) ||
                  ((MODE == KVGOV_BOUNDARY) && j == p.k && p.k > 0));
 }
 
-// PAIRS wave pairs per workgroup: waves 2p (rounds) and 2p+1 (schedule) of
-// pair p own the 64 requests blockIdx.x * 64 * PAIRS + 64 p + lane.  Trip
-// count and special iterations are decided over all pairs of the workgroup,
-// so every wave meets every barrier.
-template <int MODE, int PAIRS>
-__global__ __launch_bounds__(2 * PAIRS * kWave) void k_chains_pair(ChainArgs a) {
-  __shared__ PairLds Lp[PAIRS];
+// ---------------------------------------------------------------------------
+// lane-pair chain kernel
+// ---------------------------------------------------------------------------
+//
+// A chain is latency-bound: the 64 rounds of a compression are a dependency
+// chain, and with one lane per request a round costs its wave 14
+// instructions (plus 10 per schedule word).  This kernel takes the message
+// schedule off the rounds lanes and splits each round over two lanes.
+// Write A_t for the word a after round t and E_t for e (so b_t = A_{t-1},
+// c_t = A_{t-2}, d_t = A_{t-3}, and likewise f, g, h from E).  A round is
+//   E_{t+1} = A_{t-3} + T1_t,   T1_t = E_{t-3} + Sigma1(E_t) + Ch(E_t, E_{t-1}, E_{t-2}) + K_t + W_t
+//   A_{t+1} = T1_t + Sigma0(A_t) + Maj(A_t, A_{t-1}, A_{t-2})
+//           = E_{t+1} - A_{t-3} + Sigma0(A_t) + Maj(A_t, A_{t-1}, A_{t-2}).
+// Each request has two lanes of a rounds wave: the E lane produces the E
+// words and the A lane the A words, one round behind (in step i the E lane
+// computes E_{i+1} and the A lane A_i), so that what either lane needs from
+// its partner was produced at least one step earlier.  Both lanes run the
+// same instructions on their own last four words x0..x3 (E: E_i..E_{i-3};
+// A: A_{i-1}..A_{i-4}):
+//   S  = rotr(x0,r1) ^ rotr(x0,r2) ^ rotr(x0,r3)   Sigma1(E_i)          | Sigma0(A_{i-1})
+//   X  = bitop(x0, x1, m)                          E_i                  | ~(A_{i-1} ^ A_{i-2})
+//   F  = choose(X, x1, x2)                         Ch(E_i, .., ..)      | Maj(A_{i-1}, .., ..)
+//   Z  = (x3 ^ m) + kw                             E_{i-3} + K_i + W_i  | ~A_{i-4} + 1
+//   Z += partner's x2 (E lanes)                    + A_{i-3}            |
+//   Z += partner's x0 (A lanes)                                         | + E_i
+//   x0 = S + F + Z                                 E_{i+1}              | A_i
+// with per-lane rotation amounts, m = 0 (E) or ~0 (A), and kw = K + W on E
+// lanes and 1 on A lanes (a constant column of the LDS tables).  Choose with
+// ~(a ^ b) as selector is Maj(a, b, c).  A round is 10 instructions, and the
+// partner reads (DPP row rotations by 4 lanes under a bank mask: in each row
+// of 16 lanes, lanes 0-3 and 8-11 are E lanes and 4-7 and 12-15 their A
+// partners) are off the dependency chain.  A compression takes 65 steps: in
+// step 0 the A lane has nothing to compute (its x0 is then set to the initial
+// a, its other words start as b, c, d), and in step 64 only the A lane
+// computes (A_64).
+//
+// Workgroup: 64 requests.  Waves 0 and 1 run the rounds of 32 requests each;
+// wave 2 ("schedule", one lane per request) writes K + W of both
+// compressions to LDS tables [round][request].  Per block j, C1 = (IV;
+// h_{j-1} || T[0..7]) and C2 = (state; T[8..15] || padding):
+//   phase 1  rounds: C1 rounds 0-11      schedule: reads h_{j-1}, C1's W[16..31]
+//   phase 2  rounds: C1 rounds 12-27     schedule: C1's W[32..47]
+//   phase 3  rounds: C1 rounds 28-43     schedule: C1's W[48..63]
+//   phase 4  rounds: C1 rounds 44-63 and all of C2, then h_j to LDS and the
+//            digest; schedule: the words of block j+1 that depend on tokens
+//            only (C1 rounds 8-15, all of C2), double buffered by parity
+// with a workgroup barrier after each phase; each barrier sits four rounds
+// before the words it releases are needed, so that their LDS reads overlap
+// those rounds.  The first compression's K + W of rounds 0..7 (the words of
+// h_{j-1}) are formed by the rounds lanes from the LDS copy of h_{j-1},
+// whose constant column holds 1 - K[t], so that the A lanes' sum is 1 there
+// as well.  Iterations where some request of the workgroup has a special
+// block run on the E lanes alone (rolled compressions) while the schedule
+// wave prepares the next block.  All three waves derive trip counts and
+// special iterations from all 64 requests, so they meet the same barriers.
+
+constexpr int kLpCols = kWave + 1;  // 64 requests + the constant column
+constexpr int kLpThreads = 3 * kWave;
+
+struct LpLds {
+  uint32_t h[8][kLpCols];       // h_{j-1}; constant column: 1 - K[t]
+  uint32_t c1a[2][8][kLpCols];  // K + W of C1 rounds 8..15 (T[0..7]), by block parity
+  uint32_t c1b[48][kLpCols];    // K + W of C1 rounds 16..63
+  uint32_t c2[2][64][kLpCols];  // K + W of C2 rounds 0..63, by block parity
+};
+constexpr int kLpRows = 8 + 16 + 48 + 128;
+static_assert(sizeof(LpLds) == (size_t)kLpRows * kLpCols * 4, "LpLds rows are contiguous");
+
+struct LpLane {
+  uint32_t r1, r2, r3;  // rotation amounts of the lane's big sigma
+  uint32_t m;           // 0 on E lanes, ~0 on A lanes
+};
+
+// E lanes: the A partner's x (lane + 4, row_ror:12); A lanes: 0
+__device__ __forceinline__ uint32_t lp_from_a(uint32_t x) {
+  return __builtin_amdgcn_update_dpp(0u, x, 0x12C, 0xF, 0x5, false);
+}
+// A lanes: the E partner's x (lane - 4, row_ror:4); E lanes: 0
+__device__ __forceinline__ uint32_t lp_from_e(uint32_t x) {
+  return __builtin_amdgcn_update_dpp(0u, x, 0x124, 0xF, 0xA, false);
+}
+
+// z of a compression's step 0: (x3 ^ m) + kw_0, plus the A partner's x2 on
+// E lanes
+__device__ __forceinline__ uint32_t lp_z0(const uint32_t s[4], uint32_t kw0, const LpLane &c) {
+  uint32_t z = (s[3] ^ c.m) + kw0;
+  asm("" : "+v"(z));  // keeps the partner term one DPP add
+  return z + lp_from_a(s[2]);
+}
+
+// One step.  On entry z holds this step's (x3 ^ m) + kw plus the E lanes'
+// partner term; the step adds the A lanes' partner term, forms x0' and
+// starts the next step's z from kwn (the next step's x3 is this step's x2,
+// and its A partner's x2 is this step's x1).  Written as one block so that
+// no instruction waits on the one before it, except the first on the
+// previous step's x0; the DPP sources (x0, x1) were written at least one
+// step earlier, so the DPP reads need no wait states.
+__device__ __forceinline__ void lp_step(uint32_t s[4], uint32_t &z, uint32_t kwn,
+                                        const LpLane &c) {
+  uint32_t t1, t2, t3, x, f, sg, v, zn;
+  asm("v_alignbit_b32 %[t1], %[x0], %[x0], %[r1]\n\t"
+      "v_alignbit_b32 %[t2], %[x0], %[x0], %[r2]\n\t"
+      "v_bitop3_b32 %[x], %[x0], %[x1], %[m] bitop3:0xd2\n\t"
+      "v_alignbit_b32 %[t3], %[x0], %[x0], %[r3]\n\t"
+      "v_bitop3_b32 %[f], %[x], %[x1], %[x2] bitop3:0xca\n\t"
+      "v_bitop3_b32 %[sg], %[t1], %[t2], %[t3] bitop3:0x96\n\t"
+      "v_add_u32_dpp %[z], %[x0], %[z] row_ror:4 row_mask:0xf bank_mask:0xa\n\t"
+      "v_xad_u32 %[zn], %[x2], %[m], %[kwn]\n\t"
+      "v_add3_u32 %[v], %[sg], %[f], %[z]\n\t"
+      "v_add_u32_dpp %[zn], %[x1], %[zn] row_ror:12 row_mask:0xf bank_mask:0x5"
+      : [t1] "=&v"(t1), [t2] "=&v"(t2), [x] "=&v"(x), [t3] "=&v"(t3), [f] "=&v"(f),
+        [sg] "=&v"(sg), [z] "+&v"(z), [zn] "=&v"(zn), [v] "=&v"(v)
+      : [x0] "v"(s[0]), [x1] "v"(s[1]), [x2] "v"(s[2]), [m] "v"(c.m), [r1] "v"(c.r1),
+        [r2] "v"(c.r2), [r3] "v"(c.r3), [kwn] "v"(kwn));
+  s[3] = s[2];
+  s[2] = s[1];
+  s[1] = s[0];
+  s[0] = v;
+  z = zn;
+}
+
+// N steps; kw holds the group's own kw (kw[0] is already in z), kw_after
+// the kw of the step after the group
+template <int N>
+__device__ __forceinline__ void lp_steps(uint32_t s[4], uint32_t &z, const uint32_t *kw,
+                                         uint32_t kw_after, const LpLane &c) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) lp_step(s, z, i + 1 < N ? kw[i + 1] : kw_after, c);
+}
+
+// step 0 of a compression: the A lane's result is replaced by the initial a
+__device__ __forceinline__ void lp_first(uint32_t s[4], uint32_t &z, uint32_t kw1,
+                                         const LpLane &c, uint32_t a0, bool a_lane) {
+  lp_step(s, z, kw1, c);
+  s[0] = a_lane ? a0 : s[0];
+}
+
+// step 64: the A lane computes A_64; the E lane's words were final after
+// step 63 (e..h), the A lane's after step 64 (a..d)
+__device__ __forceinline__ void lp_last(uint32_t s[4], uint32_t &z, const LpLane &c,
+                                        bool a_lane) {
+  uint32_t e[4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x) e[x] = s[x];
+  lp_step(s, z, 1u, c);
+#pragma unroll
+  for (int x = 0; x < 4; ++x) s[x] = a_lane ? s[x] : e[x];
+}
+
+__device__ __forceinline__ void lp_load16(uint32_t w[16], const uint32_t (*rows)[kLpCols],
+                                          int base, int col) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) w[i] = rows[base + i][col];
+}
+
+// schedule words W[t0..t0+15] from the rolling window w (W[t0-16..t0-1]);
+// stores K[t0 + i] + W[t0 + i] to rows[base + i][lane]
+template <int T0>
+__device__ __forceinline__ void lp_sched16(uint32_t w[16], uint32_t (*rows)[kLpCols], int base,
+                                           int lane) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    w[i] = small_sigma1(w[(i + 14) & 15]) + w[(i + 9) & 15] + small_sigma0(w[(i + 1) & 15]) +
+           w[i];
+    rows[base + i][lane] = w[i] + kSha.K[T0 + i];
+  }
+}
+
+// K + W of block tokens Tn that depend on tokens only: C1 rounds 8..15 and
+// C2 rounds 0..7 and 16..63 (C2 rounds 8..15 are constants, set once)
+__device__ __forceinline__ void lp_prepare(const uint32_t Tn[16], LpLds &L, int buf, int lane) {
+#pragma unroll
+  for (int x = 0; x < 8; ++x) {
+    L.c1a[buf][x][lane] = kSha.K[8 + x] + Tn[x];
+    L.c2[buf][x][lane] = kSha.K[x] + Tn[8 + x];
+  }
+  uint32_t w[16];
+#pragma unroll
+  for (int x = 0; x < 8; ++x) w[x] = Tn[8 + x];
+  pad96_tail(w);
+  lp_sched16<16>(w, L.c2[buf], 16, lane);
+  lp_sched16<32>(w, L.c2[buf], 32, lane);
+  lp_sched16<48>(w, L.c2[buf], 48, lane);
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kLpThreads) void k_chains_lp(ChainArgs a) {
+  __shared__ LpLds L;
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
-  const int pair = wave >> 1;
-  const bool rounds_wave = (wave & 1) == 0;
-  PairLds &L = Lp[pair];
-  const int32_t base = blockIdx.x * kWave * PAIRS;
-  const int32_t i = base + pair * kWave + lane;
+  const bool sched_wave = wave == 2;
+  const bool a_lane = !sched_wave && ((lane >> 2) & 1);
+  const int pos = lane & 15;
+  // the request (LDS column) of this lane within the workgroup
+  const int mine =
+      sched_wave ? lane : wave * 32 + (lane >> 4) * 8 + ((pos >> 3) << 2) + (pos & 3);
+  const int32_t base = blockIdx.x * kWave;
+  const int32_t i = base + mine;
 
-  // identical set-up on both waves of a pair; a rejected or empty request
-  // has nf = 0 (both waves latch the same error, the first one wins)
   ChainReq q;
   bool ok = false;
   if (i < a.n) {
@@ -648,15 +768,13 @@ __global__ __launch_bounds__(2 * PAIRS * kWave) void k_chains_pair(ChainArgs a) 
     ok = chain_setup<MODE>(a, r, q);
   }
   const int64_t nf = ok ? q.nf : 0;
-  PairPeek peek[PAIRS];
-#pragma unroll
-  for (int p = 0; p < PAIRS; ++p)
-    peek[p] = (p == pair) ? PairPeek{nf, ok ? q.k : -1, ok && !q.salted_root}
-                          : pair_peek<MODE>(a, base + p * kWave + lane);
-  // workgroup-uniform trip count
-  int64_t J = 0;
-#pragma unroll
-  for (int p = 0; p < PAIRS; ++p) J = peek[p].nf > J ? peek[p].nf : J;
+  // Trip count and special iterations are decided over all 64 requests of
+  // the workgroup: the schedule wave holds them all, and a rounds lane also
+  // looks at the request of the same lane in the other rounds wave.
+  const ReqPeek own{nf, ok ? q.k : -1, ok && !q.salted_root};
+  ReqPeek other{0, -1, false};
+  if (!sched_wave) other = req_peek<MODE>(a, base + (1 - wave) * 32 + (mine & 31));
+  int64_t J = own.nf > other.nf ? own.nf : other.nf;
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) {
     const int64_t o = __shfl_xor(J, d, kWave);
@@ -664,138 +782,153 @@ __global__ __launch_bounds__(2 * PAIRS * kWave) void k_chains_pair(ChainArgs a) 
   }
   const bool plain_first = ok && !q.salted_root;
 
-  uint32_t H[8];
+  // constant column of every table; constant rows 8..15 of C2 (padding)
+  uint32_t(*rows)[kLpCols] = reinterpret_cast<uint32_t(*)[kLpCols]>(&L);
+  for (int x = threadIdx.x; x < kLpRows; x += kLpThreads)
+    rows[x][kWave] = x < 8 ? 1u - kShaDev.K[x] : 1u;
+  if (sched_wave) {
 #pragma unroll
-  for (int w = 0; w < 8; ++w) H[w] = (ok && q.salted_root) ? q.sig[w] : 0u;
+    for (int b = 0; b < 2; ++b) {
+      L.c2[b][8][lane] = kSha.K[8] + 0x80000000u;
+#pragma unroll
+      for (int x = 9; x < 15; ++x) L.c2[b][x][lane] = kSha.K[x];
+      L.c2[b][15][lane] = kSha.K[15] + 96 * 8;
+    }
+  }
 
-  u32x4 nxt[4];    // tokens of the next block (both waves)
-  uint32_t T[16];  // tokens of the current block
-  if (nf > 0) load_raw(q.tp, nxt);
+  // rounds lanes: role constants
+  LpLane c;
+  c.r1 = a_lane ? 2 : 6;
+  c.r2 = a_lane ? 13 : 11;
+  c.r3 = a_lane ? 22 : 25;
+  c.m = a_lane ? ~0u : 0u;
+  const int col = a_lane ? kWave : mine;
+  const int half = a_lane ? 0 : 4;  // state words held: a..d = 0..3, e..h = 4..7
+  uint32_t iv[4];  // the initial value's words held by the lane
+#pragma unroll
+  for (int x = 0; x < 4; ++x) iv[x] = a_lane ? kSha.H0[x] : kSha.H0[4 + x];
+  uint32_t iv0[4];  // step-0 registers of the first compression (A: b, c, d, -)
+#pragma unroll
+  for (int x = 0; x < 4; ++x) iv0[x] = a_lane ? (x < 3 ? kSha.H0[x + 1] : 0u) : kSha.H0[4 + x];
 
-  // prologue: h_{-1} to LDS; the schedule wave prepares C2's words of block 0
-  if (rounds_wave) {
+  u32x4 nxt[4];  // schedule wave: tokens of the next block
+  if (sched_wave) {
+    if (nf > 0) {
+      load_raw(q.tp, nxt);
+      uint32_t T0[16];
+      swap_block(nxt, T0);
+      lp_prepare(T0, L, 0, lane);
+    }
+  } else if (!a_lane && ok) {
+    // h_{-1}: sigma for a root-salted first block, else unused
 #pragma unroll
-    for (int w = 0; w < 8; ++w) L.h[w][lane] = H[w];
-  } else if (nf > 0) {
-    uint32_t T0[16];
-    swap_block(nxt, T0);
-    uint32_t w[16];
-#pragma unroll
-    for (int x = 0; x < 8; ++x) w[x] = T0[8 + x];
-    pad96_tail(w);
-    sched16(w, L.w2[0], 0, lane);
-    sched16(w, L.w2[0], 16, lane);
-    sched16(w, L.w2[0], 32, lane);
+    for (int w = 0; w < 8; ++w) L.h[w][mine] = q.salted_root ? q.sig[w] : 0u;
   }
   __syncthreads();
 
   for (int64_t j = 0; j < J; ++j) {
     const bool act = j < nf;
-    if (act) {
-      swap_block(nxt, T);
-      if (j + 1 < nf) load_raw(q.tp + 16 * (j + 1), nxt);
-    }
-    const bool u0 = act && plain_first && j == 0;
-    const bool bnd = act && (MODE == KVGOV_BOUNDARY) && j == q.k && q.k > 0;
-    const int nb = (int)((j + 1) & 1);  // C2 buffer of block j+1
     const bool next = j + 1 < nf;
+    const int cb = (int)(j & 1), nb = cb ^ 1;
+    uint32_t T[16];  // schedule wave: tokens of block j
+    if (sched_wave && act) take_block(nxt, T, q.tp, j, nf);
 
     bool special_any = false;
-    if (MODE != KVGOV_ROOT) {
-#pragma unroll
-      for (int p = 0; p < PAIRS; ++p) special_any |= pair_special<MODE>(peek[p], j);
-    }
+    if (MODE != KVGOV_ROOT)
+      special_any = req_special<MODE>(own, j) || req_special<MODE>(other, j);
     if (MODE != KVGOV_ROOT && __any(special_any)) {
-      // special iteration: the rounds wave does the whole block itself
-      if (rounds_wave) {
-        if (act) {
-          special_block(H, T, q.sig, u0, bnd);
-#pragma unroll
-          for (int w = 0; w < 8; ++w) L.h[w][lane] = H[w];
-          store_digest(q.out + j * 32, H);
+      // special iteration: the E lane of every request does its whole block
+      if (sched_wave) {
+        if (next) {
+          uint32_t Tn[16];
+          swap_block(nxt, Tn);
+          lp_prepare(Tn, L, nb, lane);
         }
-      } else if (next) {
-        uint32_t Tn[16], w[16];
-        swap_block(nxt, Tn);
+      } else if (act && !a_lane) {
+        const bool u0 = plain_first && j == 0;
+        const bool bnd = (MODE == KVGOV_BOUNDARY) && j == q.k && q.k > 0;
+        u32x4 raw[4];
+        uint32_t H[8], Tb[16];
+        load_raw(q.tp + 16 * j, raw);
+        swap_block(raw, Tb);
 #pragma unroll
-        for (int x = 0; x < 8; ++x) w[x] = Tn[8 + x];
-        pad96_tail(w);
-        sched16(w, L.w2[nb], 0, lane);
-        sched16(w, L.w2[nb], 16, lane);
-        sched16(w, L.w2[nb], 32, lane);
+        for (int w = 0; w < 8; ++w) H[w] = L.h[w][mine];
+        special_block(H, Tb, q.sig, u0, bnd);
+#pragma unroll
+        for (int w = 0; w < 8; ++w) L.h[w][mine] = H[w];
+        store_digest(q.out + j * 32, H);
       }
       __syncthreads();
       continue;
     }
 
-    if (rounds_wave) {
-      // Each barrier sits 4 rounds before the words it releases are needed,
-      // so the LDS reads issued right after it overlap those 4 rounds; the
-      // scheduling barriers keep the compiler from sinking the reads to
-      // their uses.  C2's words (written during the previous block) are read
-      // one group ahead.
-      Sha8 s = sha8_iv();
-      uint32_t wa[16], wb[16];
+    if (!sched_wave) {
+      // ---- rounds waves.  Step i of a group takes the kw of step i + 1 (the
+      // next step's z starts early).
+      uint32_t s[4], st[4], wa[16], wb[16], z = 0;
       if (act) {
+        uint32_t kw8[8];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) round_w(s, kSha.K[t], H[t]);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) round_w(s, kSha.K[8 + t], T[t]);
-      }
-      __syncthreads();  // C1 W[16..31] ready
-      if (act) {
-        load16(wa, L.w1, 0, lane);
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int t = 4; t < 8; ++t) round_w(s, kSha.K[8 + t], T[t]);
-        rounds12(s, wa, 16);
-      }
-      __syncthreads();  // C1 W[32..47] ready
-      if (act) {
-        load16(wb, L.w1, 16, lane);
-        __builtin_amdgcn_sched_barrier(0);
-        rounds4(s, wa + 12, 28);
-        rounds12(s, wb, 32);
-      }
-      __syncthreads();  // C1 W[48..63] ready
-      if (act) {
-        const uint32_t(*w2)[kWave] = L.w2[j & 1];
-        load16(wa, L.w1, 32, lane);
-        __builtin_amdgcn_sched_barrier(0);
-        rounds4(s, wb + 12, 44);
-        load16(wb, w2, 0, lane);  // C2 W[16..31]
-        __builtin_amdgcn_sched_barrier(0);
-        rounds12(s, wa, 48);
-        rounds4(s, wa + 12, 60);
-        uint32_t st[8];
-#pragma unroll
-        for (int w = 0; w < 8; ++w) st[w] = kSha.H0[w];
-        sha8_add(st, s);
-        // C2: rounds 0-15 from registers (T[8..15] || pad96), 16-63 from LDS
-        Sha8 s2 = sha8_load(st);
-        load16(wa, w2, 16, lane);  // C2 W[32..47]
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int t = 0; t < 8; ++t) round_w(s2, kSha.K[t], T[8 + t]);
-        round_w(s2, kSha.K[8], 0x80000000u);
-#pragma unroll
-        for (int t = 9; t < 15; ++t) round_w(s2, kSha.K[t], 0u);
-        round_w(s2, kSha.K[15], 96 * 8);
-        rounds12(s2, wb, 16);
-        rounds4(s2, wb + 12, 28);
-        load16(wb, w2, 32, lane);  // C2 W[48..63]
-        __builtin_amdgcn_sched_barrier(0);
-        rounds12(s2, wa, 32);
-        rounds4(s2, wa + 12, 44);
-        rounds12(s2, wb, 48);
-        rounds4(s2, wb + 12, 60);
-        sha8_add(st, s2);
-#pragma unroll
-        for (int w = 0; w < 8; ++w) {
-          H[w] = st[w];
-          L.h[w][lane] = st[w];
+        for (int t = 0; t < 8; ++t) {
+          kw8[t] = kSha.K[t] + L.h[t][col];
+          wa[8 + t] = L.c1a[cb][t][col];
         }
-        store_digest(q.out + j * 32, H);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) s[x] = iv0[x];
+        z = lp_z0(s, kw8[0], c);
+        lp_first(s, z, kw8[1], c, kSha.H0[0], a_lane);
+        lp_steps<7>(s, z, kw8 + 1, wa[8], c);    // rounds 1..7
+        lp_steps<4>(s, z, wa + 8, wa[12], c);    // 8..11
+      }
+      __syncthreads();  // C1 rounds 16..31 ready
+      if (act) {
+        lp_load16(wb, L.c1b, 0, col);
+        __builtin_amdgcn_sched_barrier(0);
+        lp_steps<4>(s, z, wa + 12, wb[0], c);    // 12..15
+        lp_steps<12>(s, z, wb, wb[12], c);       // 16..27
+      }
+      __syncthreads();  // C1 rounds 32..47 ready
+      if (act) {
+        lp_load16(wa, L.c1b, 16, col);
+        __builtin_amdgcn_sched_barrier(0);
+        lp_steps<4>(s, z, wb + 12, wa[0], c);    // 28..31
+        lp_steps<12>(s, z, wa, wa[12], c);       // 32..43
+      }
+      __syncthreads();  // C1 rounds 48..63 ready
+      if (act) {
+        lp_load16(wb, L.c1b, 32, col);
+        __builtin_amdgcn_sched_barrier(0);
+        lp_steps<4>(s, z, wa + 12, wb[0], c);    // 44..47
+        lp_load16(wa, L.c2[cb], 0, col);
+        __builtin_amdgcn_sched_barrier(0);
+        lp_steps<16>(s, z, wb, 1u, c);           // 48..63
+        lp_last(s, z, c, a_lane);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) st[x] = iv[x] + s[x];
+        // C2 step-0 registers: E: e, f, g, h; A: b, c, d, -
+#pragma unroll
+        for (int x = 0; x < 4; ++x) s[x] = a_lane ? (x < 3 ? st[x + 1] : 0u) : st[x];
+        z = lp_z0(s, wa[0], c);
+        lp_load16(wb, L.c2[cb], 16, col);
+        __builtin_amdgcn_sched_barrier(0);
+        lp_first(s, z, wa[1], c, st[0], a_lane);
+        lp_steps<15>(s, z, wa + 1, wb[0], c);    // C2 1..15
+        lp_load16(wa, L.c2[cb], 32, col);
+        __builtin_amdgcn_sched_barrier(0);
+        lp_steps<16>(s, z, wb, wa[0], c);        // 16..31
+        lp_load16(wb, L.c2[cb], 48, col);
+        __builtin_amdgcn_sched_barrier(0);
+        lp_steps<16>(s, z, wa, wb[0], c);        // 32..47
+        lp_steps<16>(s, z, wb, 1u, c);           // 48..63
+        lp_last(s, z, c, a_lane);
+        uint32_t o[4];
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          o[x] = st[x] + s[x];
+          L.h[half + x][mine] = o[x];
+        }
+        u32x4 *dst = reinterpret_cast<u32x4 *>(q.out + j * 32 + half * 4);
+        *dst = u32x4{bswap(o[0]), bswap(o[1]), bswap(o[2]), bswap(o[3])};
       }
       __syncthreads();
     } else {
@@ -803,23 +936,21 @@ __global__ __launch_bounds__(2 * PAIRS * kWave) void k_chains_pair(ChainArgs a) 
       uint32_t w[16];
       if (act) {
 #pragma unroll
-        for (int x = 0; x < 8; ++x) { w[x] = L.h[x][lane]; w[8 + x] = T[x]; }
-        sched16(w, L.w1, 0, lane);
+        for (int x = 0; x < 8; ++x) {
+          w[x] = L.h[x][lane];
+          w[8 + x] = T[x];
+        }
+        lp_sched16<16>(w, L.c1b, 0, lane);
       }
       __syncthreads();
-      if (act) sched16(w, L.w1, 16, lane);
+      if (act) lp_sched16<32>(w, L.c1b, 16, lane);
       __syncthreads();
-      if (act) sched16(w, L.w1, 32, lane);
+      if (act) lp_sched16<48>(w, L.c1b, 32, lane);
       __syncthreads();
       if (next) {
         uint32_t Tn[16];
         swap_block(nxt, Tn);
-#pragma unroll
-        for (int x = 0; x < 8; ++x) w[x] = Tn[8 + x];
-        pad96_tail(w);
-        sched16(w, L.w2[nb], 0, lane);
-        sched16(w, L.w2[nb], 16, lane);
-        sched16(w, L.w2[nb], 32, lane);
+        lp_prepare(Tn, L, nb, lane);
       }
       __syncthreads();
     }
@@ -861,26 +992,25 @@ static int cu_lds_bytes() {
   return v;
 }
 
-// Dynamic LDS of a wave-pair workgroup so that at most `per_cu` pair
-// workgroups share a CU (1: more than half of the CU's LDS; 2: more than a
-// third, at most half).
-static size_t pair_lds_reserve(int per_cu) {
+// Dynamic LDS of a lane-pair workgroup so that at most `per_cu` of them
+// share a CU.
+static size_t lp_lds_reserve(int per_cu) {
   const size_t cu = (size_t)cu_lds_bytes();
   const size_t want = per_cu == 1 ? cu / 2 + 4096 : cu / 2 - 1024;
-  const size_t fixed = KVGOV_PAIRS * sizeof(PairLds);
-  return want > fixed ? want - fixed : 0;
+  return want > sizeof(LpLds) ? want - sizeof(LpLds) : 0;
 }
 
-// Pair workgroups per CU for a batch of n requests: the wave-pair kernel
-// shortens every chain but needs two waves per 64 requests, so it runs while
-// the batch fits in one or two pairs per CU (latency-bound batches); larger
-// batches keep every SIMD busy with the single-wave kernel (0).
-static int pair_slots(int32_t n) {
-  if (!KVGOV_PAIR_DEFAULT || n <= 0) return 0;
-  const int64_t pairs = ceil_div(n, (int64_t)kWave * KVGOV_PAIRS);
+// Lane-pair workgroups per CU for a batch of n requests: the lane-pair
+// kernel shortens every chain but needs three waves per 64 requests, so it
+// runs while the batch fits in one or two workgroups per CU (latency-bound
+// batches); larger batches keep every SIMD busy with the single-wave kernel
+// (0).
+static int lp_slots(int32_t n) {
+  if (!KVGOV_LANE_PAIR || n <= 0) return 0;
+  const int64_t groups = ceil_div(n, (int64_t)kWave);
   const int64_t cus = device_cu_count();
-  if (pairs <= cus) return 1;
-  if (pairs <= 2 * cus) return 2;
+  if (groups <= cus) return 1;
+  if (groups <= 2 * cus) return 2;
   return 0;
 }
 
@@ -972,7 +1102,7 @@ int kvgov_block_offsets(const int64_t *tok_offsets, int32_t n, int32_t block_siz
 // Longest-first ordering pays once the batch has about as many waves as the
 // chip has SIMDs; below that every wave has a SIMD of its own from the start
 // and the kernel takes as long as its longest chain in any order.  (Batches
-// that run on the wave-pair kernel are resident all at once and are never
+// that run on the lane-pair kernel are resident all at once and are never
 // ordered.)
 static int64_t order_min_requests() { return (int64_t)device_cu_count() * 4 * kWave / 2; }
 
@@ -1008,7 +1138,7 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
   a.status = status;
   a.order = nullptr;
 
-  const int slots = pair_slots(n);
+  const int slots = lp_slots(n);
   int32_t *scratch = nullptr;
   if (!slots && n >= order_min_requests()) {
     const size_t bytes = sizeof(int32_t) * ((size_t)kOrderBuckets + (size_t)n);
@@ -1031,14 +1161,14 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
   // then takes nearly every issue slot, so the workgroups reserve LDS (unused
   // beyond the kernel's own) to bound how many share a CU.
   if (slots) {
-    // wave pairs (rounds wave + schedule wave), one or two pairs per CU
-    constexpr int P = KVGOV_PAIRS;
-    const dim3 grid((unsigned)ceil_div(n, kWave * P)), block(2 * P * kWave);
-    const size_t lds = pair_lds_reserve(slots);
+    // lane pairs: two rounds waves and a schedule wave per 64 requests, one
+    // or two workgroups per CU
+    const dim3 grid((unsigned)ceil_div(n, kWave)), block(kLpThreads);
+    const size_t lds = lp_lds_reserve(slots);
     switch (mode) {
-      case KVGOV_NONE: hipLaunchKernelGGL((k_chains_pair<KVGOV_NONE, P>), grid, block, lds, s, a); break;
-      case KVGOV_ROOT: hipLaunchKernelGGL((k_chains_pair<KVGOV_ROOT, P>), grid, block, lds, s, a); break;
-      default: hipLaunchKernelGGL((k_chains_pair<KVGOV_BOUNDARY, P>), grid, block, lds, s, a); break;
+      case KVGOV_NONE: hipLaunchKernelGGL(k_chains_lp<KVGOV_NONE>, grid, block, lds, s, a); break;
+      case KVGOV_ROOT: hipLaunchKernelGGL(k_chains_lp<KVGOV_ROOT>, grid, block, lds, s, a); break;
+      default: hipLaunchKernelGGL(k_chains_lp<KVGOV_BOUNDARY>, grid, block, lds, s, a); break;
     }
   } else {
     // at most one workgroup per CU; batches of at most one wave per CU run

@@ -109,3 +109,23 @@ def test_binding_fails_loudly_without_gpu():
         pytest.skip("a GPU is present")
     with pytest.raises((ValueError, RuntimeError)):
         K.salts(b"k" * 32, torch.zeros((2, 32), dtype=torch.uint8))
+
+
+def test_peaks_library_exports_and_validates():
+    from paper_2608_09225_amd import peaks as P
+    if not os.path.exists(P.LIB_PATH):
+        pytest.skip("libkvgov_peaks.so not built")
+    with open(P.HEADER_PATH) as f:
+        text = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+    names = sorted(set(re.findall(r"\b(kvgov_\w+)\s*\(", text)))
+    assert names == sorted(P._SIGNATURES)
+    L = P.lib()
+    inval = int(re.search(r"KVGOV_PEAK_E_INVAL\s+\((-?\d+)\)", text).group(1))
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+    n = ctypes.c_int64()
+    assert L.kvgov_peak_valu(None, 4, 4, ctypes.byref(n), None) == inval
+    assert L.kvgov_peak_valu(fake, 0, 4, ctypes.byref(n), None) == inval
+    assert L.kvgov_peak_gather(fake, 3, fake, 4, 4, ctypes.byref(n), None) == inval
+    assert L.kvgov_peak_gather(fake, 0, fake, 4, 4, ctypes.byref(n), None) == inval
+    assert L.kvgov_peak_gather(ctypes.c_void_p(0x1008), 16, fake, 4, 4, ctypes.byref(n),
+                               None) == inval
