@@ -565,8 +565,9 @@ def main():
         waves = int(np.ceil(X.n / 64))  # one lane per request
         cus = torch.cuda.get_device_properties(dev).multi_processor_count
         # the library's launch policy: the lane-pair kernel while the batch
-        # fits in two 64-request workgroups per CU
-        kname = "k_chains_lp" if X.n <= 2 * 64 * cus else "k_chains"
+        # fits in two 64-request workgroups per CU, else the mixed kernel
+        # (longest requests on lane-pair workgroups, the rest one lane each)
+        kname = "k_chains_lp" if X.n <= 2 * 64 * cus else "k_chains_mixed"
         tr = {m: recorded_traffic(f"{kname}<{m}>", wl.name, "chains") for m in modes}
         traffic = None
         if all(t is not None for t in tr.values()):

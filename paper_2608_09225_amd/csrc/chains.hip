@@ -486,8 +486,7 @@ __device__ __forceinline__ void pad96_tail(uint32_t w[16]) {
 // One lane per request.  Every instruction of a compression (rounds and
 // message schedule) is issued by the lane's wave.
 template <int MODE>
-__global__ __launch_bounds__(256) void k_chains(ChainArgs a) {
-  const int32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+__device__ __forceinline__ void single_chain(const ChainArgs &a, int32_t i) {
   if (i >= a.n) return;
   const int32_t r = a.order ? a.order[i] : i;
   ChainReq q;
@@ -529,6 +528,11 @@ __global__ __launch_bounds__(256) void k_chains(ChainArgs a) {
     take_block(nxt, T, q.tp, j + 1 < nf ? j + 1 : j, nf);
     store_digest(q.out + j * 32, H);
   }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(256) void k_chains(ChainArgs a) {
+  single_chain<MODE>(a, blockIdx.x * blockDim.x + threadIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -747,18 +751,21 @@ __device__ __forceinline__ void lp_prepare(const uint32_t Tn[16], LpLds &L, int 
   lp_sched16<48>(w, L.c2[buf], 48, lane);
 }
 
+// Workgroup `group` of the lane-pair kernel: requests group * 64 + 0..63 of
+// the (ordered) batch.  Waves 0 and 1 run the rounds, wave 2 the schedule; a
+// fourth wave (workgroups of 256 lanes) only keeps the barriers.
 template <int MODE>
-__global__ __launch_bounds__(kLpThreads) void k_chains_lp(ChainArgs a) {
-  __shared__ LpLds L;
+__device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLds &L) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
-  const bool sched_wave = wave == 2;
+  const bool sched_wave = wave >= 2;
+  const bool idle = wave >= 3;
   const bool a_lane = !sched_wave && ((lane >> 2) & 1);
   const int pos = lane & 15;
   // the request (LDS column) of this lane within the workgroup
   const int mine =
       sched_wave ? lane : wave * 32 + (lane >> 4) * 8 + ((pos >> 3) << 2) + (pos & 3);
-  const int32_t base = blockIdx.x * kWave;
+  const int32_t base = group * kWave;
   const int32_t i = base + mine;
 
   ChainReq q;
@@ -784,9 +791,9 @@ __global__ __launch_bounds__(kLpThreads) void k_chains_lp(ChainArgs a) {
 
   // constant column of every table; constant rows 8..15 of C2 (padding)
   uint32_t(*rows)[kLpCols] = reinterpret_cast<uint32_t(*)[kLpCols]>(&L);
-  for (int x = threadIdx.x; x < kLpRows; x += kLpThreads)
+  for (int x = threadIdx.x; x < kLpRows; x += blockDim.x)
     rows[x][kWave] = x < 8 ? 1u - kShaDev.K[x] : 1u;
-  if (sched_wave) {
+  if (sched_wave && !idle) {
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       L.c2[b][8][lane] = kSha.K[8] + 0x80000000u;
@@ -813,7 +820,7 @@ __global__ __launch_bounds__(kLpThreads) void k_chains_lp(ChainArgs a) {
 
   u32x4 nxt[4];  // schedule wave: tokens of the next block
   if (sched_wave) {
-    if (nf > 0) {
+    if (nf > 0 && !idle) {
       load_raw(q.tp, nxt);
       uint32_t T0[16];
       swap_block(nxt, T0);
@@ -831,7 +838,7 @@ __global__ __launch_bounds__(kLpThreads) void k_chains_lp(ChainArgs a) {
     const bool next = j + 1 < nf;
     const int cb = (int)(j & 1), nb = cb ^ 1;
     uint32_t T[16];  // schedule wave: tokens of block j
-    if (sched_wave && act) take_block(nxt, T, q.tp, j, nf);
+    if (sched_wave && act && !idle) take_block(nxt, T, q.tp, j, nf);
 
     bool special_any = false;
     if (MODE != KVGOV_ROOT)
@@ -839,7 +846,7 @@ __global__ __launch_bounds__(kLpThreads) void k_chains_lp(ChainArgs a) {
     if (MODE != KVGOV_ROOT && __any(special_any)) {
       // special iteration: the E lane of every request does its whole block
       if (sched_wave) {
-        if (next) {
+        if (next && !idle) {
           uint32_t Tn[16];
           swap_block(nxt, Tn);
           lp_prepare(Tn, L, nb, lane);
@@ -932,9 +939,9 @@ __global__ __launch_bounds__(kLpThreads) void k_chains_lp(ChainArgs a) {
       }
       __syncthreads();
     } else {
-      // ---- schedule wave
+      // ---- schedule wave (an idle wave only meets the barriers)
       uint32_t w[16];
-      if (act) {
+      if (act && !idle) {
 #pragma unroll
         for (int x = 0; x < 8; ++x) {
           w[x] = L.h[x][lane];
@@ -943,11 +950,11 @@ __global__ __launch_bounds__(kLpThreads) void k_chains_lp(ChainArgs a) {
         lp_sched16<16>(w, L.c1b, 0, lane);
       }
       __syncthreads();
-      if (act) lp_sched16<32>(w, L.c1b, 16, lane);
+      if (act && !idle) lp_sched16<32>(w, L.c1b, 16, lane);
       __syncthreads();
-      if (act) lp_sched16<48>(w, L.c1b, 32, lane);
+      if (act && !idle) lp_sched16<48>(w, L.c1b, 32, lane);
       __syncthreads();
-      if (next) {
+      if (next && !idle) {
         uint32_t Tn[16];
         swap_block(nxt, Tn);
         lp_prepare(Tn, L, nb, lane);
@@ -955,6 +962,27 @@ __global__ __launch_bounds__(kLpThreads) void k_chains_lp(ChainArgs a) {
       __syncthreads();
     }
   }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kLpThreads) void k_chains_lp(ChainArgs a) {
+  __shared__ LpLds L;
+  lp_group<MODE>(a, blockIdx.x, L);
+}
+
+// Large ordered batches: the first `lp_groups` workgroups run the lane-pair
+// path on the longest requests (the batch is ordered longest first), so
+// that the longest chains finish ~1.4x sooner; the remaining workgroups run
+// one lane per request on the rest.  Both in one launch, 256 lanes per
+// workgroup.
+template <int MODE>
+__global__ __launch_bounds__(256) void k_chains_mixed(ChainArgs a, int32_t lp_groups) {
+  __shared__ LpLds L;
+  if ((int32_t)blockIdx.x < lp_groups)
+    lp_group<MODE>(a, blockIdx.x, L);
+  else
+    single_chain<MODE>(a, lp_groups * kWave + ((int32_t)blockIdx.x - lp_groups) * 256 +
+                              (int32_t)threadIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -1169,6 +1197,19 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
       case KVGOV_NONE: hipLaunchKernelGGL(k_chains_lp<KVGOV_NONE>, grid, block, lds, s, a); break;
       case KVGOV_ROOT: hipLaunchKernelGGL(k_chains_lp<KVGOV_ROOT>, grid, block, lds, s, a); break;
       default: hipLaunchKernelGGL(k_chains_lp<KVGOV_BOUNDARY>, grid, block, lds, s, a); break;
+    }
+  } else if (a.order && KVGOV_LANE_PAIR) {
+    // ordered batch: the longest requests on lane-pair workgroups (one
+    // eighth of the CUs), the rest one lane per request; one workgroup per CU
+    const int32_t lp_groups = std::max(1, device_cu_count() / 8);
+    const int64_t rest = std::max<int64_t>(0, (int64_t)n - (int64_t)lp_groups * kWave);
+    const dim3 grid((unsigned)(lp_groups + ceil_div(rest, 4 * kWave))), block(4 * kWave);
+    const size_t res = chain_lds_reserve();
+    const size_t lds = res > sizeof(LpLds) ? res - sizeof(LpLds) : 0;
+    switch (mode) {
+      case KVGOV_NONE: hipLaunchKernelGGL(k_chains_mixed<KVGOV_NONE>, grid, block, lds, s, a, lp_groups); break;
+      case KVGOV_ROOT: hipLaunchKernelGGL(k_chains_mixed<KVGOV_ROOT>, grid, block, lds, s, a, lp_groups); break;
+      default: hipLaunchKernelGGL(k_chains_mixed<KVGOV_BOUNDARY>, grid, block, lds, s, a, lp_groups); break;
     }
   } else {
     // at most one workgroup per CU; batches of at most one wave per CU run
