@@ -44,6 +44,9 @@
 #ifndef KVGOV_LANE_PAIR
 #define KVGOV_LANE_PAIR 1  // 0: the single-wave kernel for every batch
 #endif
+#ifndef KVGOV_LP_COVER
+#define KVGOV_LP_COVER 2  // lane-pair kernel: steps between a barrier and its first word
+#endif
 
 namespace kvgov {
 
@@ -539,31 +542,23 @@ __global__ __launch_bounds__(256) void k_chains(ChainArgs a) {
 // helpers of the lane-pair kernel
 // ---------------------------------------------------------------------------
 
-// Block-count summary of a request, used to keep the waves of a workgroup in
-// lockstep: every wave decides trip counts and special iterations over all
-// requests of the workgroup.
+// Block count and boundary block of a request, used to keep the waves of a
+// workgroup in lockstep: every wave decides trip counts and boundary
+// iterations over all requests of the workgroup.
 struct ReqPeek {
   int64_t nf;
   int64_t k;
-  bool plain_first;
 };
 
 template <int MODE>
 __device__ __forceinline__ ReqPeek req_peek(const ChainArgs &a, int32_t i) {
-  ReqPeek p{0, -1, false};
+  ReqPeek p{0, -1};
   if (i < a.n) {
     ChainReq q;
     const int32_t r = a.order ? a.order[i] : i;
-    if (chain_setup<MODE>(a, r, q)) p = ReqPeek{q.nf, q.k, !q.salted_root};
+    if (chain_setup<MODE>(a, r, q)) p = ReqPeek{q.nf, q.k};
   }
   return p;
-}
-
-template <int MODE>
-__device__ __forceinline__ bool req_special(const ReqPeek &p, int64_t j) {
-  const bool act = j < p.nf;
-  return act && ((p.plain_first && j == 0) ||
-                 ((MODE == KVGOV_BOUNDARY) && j == p.k && p.k > 0));
 }
 
 // ---------------------------------------------------------------------------
@@ -579,28 +574,26 @@ __device__ __forceinline__ bool req_special(const ReqPeek &p, int64_t j) {
 //   E_{t+1} = A_{t-3} + T1_t,   T1_t = E_{t-3} + Sigma1(E_t) + Ch(E_t, E_{t-1}, E_{t-2}) + K_t + W_t
 //   A_{t+1} = T1_t + Sigma0(A_t) + Maj(A_t, A_{t-1}, A_{t-2})
 //           = E_{t+1} - A_{t-3} + Sigma0(A_t) + Maj(A_t, A_{t-1}, A_{t-2}).
-// Each request has two lanes of a rounds wave: the E lane produces the E
-// words and the A lane the A words, one round behind (in step i the E lane
-// computes E_{i+1} and the A lane A_i), so that what either lane needs from
-// its partner was produced at least one step earlier.  Both lanes run the
-// same instructions on their own last four words x0..x3 (E: E_i..E_{i-3};
-// A: A_{i-1}..A_{i-4}):
-//   S  = rotr(x0,r1) ^ rotr(x0,r2) ^ rotr(x0,r3)   Sigma1(E_i)          | Sigma0(A_{i-1})
-//   X  = bitop(x0, x1, m)                          E_i                  | ~(A_{i-1} ^ A_{i-2})
-//   F  = choose(X, x1, x2)                         Ch(E_i, .., ..)      | Maj(A_{i-1}, .., ..)
-//   Z  = (x3 ^ m) + kw                             E_{i-3} + K_i + W_i  | ~A_{i-4} + 1
-//   Z += partner's x2 (E lanes)                    + A_{i-3}            |
-//   Z += partner's x0 (A lanes)                                         | + E_i
-//   x0 = S + F + Z                                 E_{i+1}              | A_i
+// Each request has two adjacent lanes of a rounds wave: the E lane (even)
+// produces the E words and the A lane (odd) the A words, two rounds behind:
+// in step i the E lane computes E_{i+1} and the A lane A_{i-1}.  Both run the
+// same nine instructions on their own last four words x0..x3 (E: E_i..E_{i-3};
+// A: A_{i-2}..A_{i-5}), and each needs its partner's x1 (A_{i-3} resp.
+// E_{i-1}), which one DPP quad swap delivers to both:
+//   S  = rotr(x0,r1) ^ rotr(x0,r2) ^ rotr(x0,r3)   Sigma1(E_i)          | Sigma0(A_{i-2})
+//   X  = bitop(x0, x1, m)                          E_i                  | ~(A_{i-2} ^ A_{i-3})
+//   F  = choose(X, x1, x2)                         Ch(E_i, .., ..)      | Maj(A_{i-2}, .., ..)
+//   Z  = (x3 ^ m) + kw + partner's x1              E_{i-3} + K_i + W_i  | ~A_{i-5} + 1 + E_{i-1}
+//                                                  + A_{i-3}            |
+//   x0 = S + F + Z                                 E_{i+1}              | A_{i-1}
 // with per-lane rotation amounts, m = 0 (E) or ~0 (A), and kw = K + W on E
 // lanes and 1 on A lanes (a constant column of the LDS tables).  Choose with
-// ~(a ^ b) as selector is Maj(a, b, c).  A round is 10 instructions, and the
-// partner reads (DPP row rotations by 4 lanes under a bank mask: in each row
-// of 16 lanes, lanes 0-3 and 8-11 are E lanes and 4-7 and 12-15 their A
-// partners) are off the dependency chain.  A compression takes 65 steps: in
-// step 0 the A lane has nothing to compute (its x0 is then set to the initial
-// a, its other words start as b, c, d), and in step 64 only the A lane
-// computes (A_64).
+// ~(a ^ b) as selector is Maj(a, b, c).  Z depends only on words from
+// earlier steps, so it is formed one step ahead, and the DPP read is off the
+// dependency chain (x0 -> rotates -> xor3 -> add3, and x0 -> X -> choose).
+// A compression takes 66 steps: in steps 0 and 1 the A lane has nothing to
+// compute (its x0 is then set to the initial b, then a; it starts from c, d),
+// and in steps 64 and 65 only the A lane computes (A_63, A_64).
 //
 // Workgroup: 64 requests.  Waves 0 and 1 run the rounds of 32 requests each;
 // wave 2 ("schedule", one lane per request) writes K + W of both
@@ -626,65 +619,106 @@ constexpr int kLpCols = kWave + 1;  // 64 requests + the constant column
 constexpr int kLpThreads = 3 * kWave;
 
 struct LpLds {
-  uint32_t h[8][kLpCols];       // h_{j-1}; constant column: 1 - K[t]
-  uint32_t c1a[2][8][kLpCols];  // K + W of C1 rounds 8..15 (T[0..7]), by block parity
-  uint32_t c1b[48][kLpCols];    // K + W of C1 rounds 16..63
-  uint32_t c2[2][64][kLpCols];  // K + W of C2 rounds 0..63, by block parity
+  uint32_t ha[8][kLpCols];      // message words 0..7 of the first compression;
+                                // constant column: 1 - K[t]
+  uint32_t hb[8][kLpCols];      // message words 8..15; constant column: 1 - K[8 + t]
+  uint32_t c1b[48][kLpCols];    // K + W of the first compression, rounds 16..63
+  uint32_t c2[2][64][kLpCols];  // K + W of the second compression, by block parity
+  uint32_t c3[64][2];           // K + W of a 128-byte message's padding block; [.][1] = 1
 };
-constexpr int kLpRows = 8 + 16 + 48 + 128;
-static_assert(sizeof(LpLds) == (size_t)kLpRows * kLpCols * 4, "LpLds rows are contiguous");
+constexpr int kLpRows = 8 + 8 + 48 + 128;  // rows with a constant column
+static_assert(sizeof(LpLds) == (size_t)kLpRows * kLpCols * 4 + 64 * 2 * 4,
+              "LpLds rows are contiguous");
+
+// K + W of the padding block of a 128-byte message (constant), from the
+// schedule's definition
+struct PadSchedule {
+  uint32_t kw[64];
+};
+constexpr uint32_t c_rotr(uint32_t x, int n) { return (x >> n) | (x << (32 - n)); }
+constexpr PadSchedule make_pad128_schedule() {
+  PadSchedule p{};
+  uint32_t w[64] = {};
+  w[0] = 0x80000000u;
+  w[15] = 128 * 8;
+  for (int t = 16; t < 64; ++t) {
+    const uint32_t s0 = c_rotr(w[t - 15], 7) ^ c_rotr(w[t - 15], 18) ^ (w[t - 15] >> 3);
+    const uint32_t s1 = c_rotr(w[t - 2], 17) ^ c_rotr(w[t - 2], 19) ^ (w[t - 2] >> 10);
+    w[t] = s1 + w[t - 7] + s0 + w[t - 16];
+  }
+  for (int t = 0; t < 64; ++t) p.kw[t] = kSha.K[t] + w[t];
+  return p;
+}
+__constant__ PadSchedule kPad128Dev = make_pad128_schedule();
 
 struct LpLane {
   uint32_t r1, r2, r3;  // rotation amounts of the lane's big sigma
   uint32_t m;           // 0 on E lanes, ~0 on A lanes
 };
 
-// E lanes: the A partner's x (lane + 4, row_ror:12); A lanes: 0
-__device__ __forceinline__ uint32_t lp_from_a(uint32_t x) {
-  return __builtin_amdgcn_update_dpp(0u, x, 0x12C, 0xF, 0x5, false);
-}
-// A lanes: the E partner's x (lane - 4, row_ror:4); E lanes: 0
-__device__ __forceinline__ uint32_t lp_from_e(uint32_t x) {
-  return __builtin_amdgcn_update_dpp(0u, x, 0x124, 0xF, 0xA, false);
+// the partner lane's x (adjacent lanes swap: DPP quad_perm [1,0,3,2])
+__device__ __forceinline__ uint32_t lp_partner(uint32_t x) {
+  return __builtin_amdgcn_update_dpp(0u, x, 0xB1, 0xF, 0xF, false);
 }
 
-// z of a compression's step 0: (x3 ^ m) + kw_0, plus the A partner's x2 on
-// E lanes
+// z of a compression's step 0: (x3 ^ m) + kw_0 + the partner's x1
 __device__ __forceinline__ uint32_t lp_z0(const uint32_t s[4], uint32_t kw0, const LpLane &c) {
   uint32_t z = (s[3] ^ c.m) + kw0;
   asm("" : "+v"(z));  // keeps the partner term one DPP add
-  return z + lp_from_a(s[2]);
+  return z + lp_partner(s[1]);
 }
 
-// One step.  On entry z holds this step's (x3 ^ m) + kw plus the E lanes'
-// partner term; the step adds the A lanes' partner term, forms x0' and
-// starts the next step's z from kwn (the next step's x3 is this step's x2,
-// and its A partner's x2 is this step's x1).  Written as one block so that
-// no instruction waits on the one before it, except the first on the
-// previous step's x0; the DPP sources (x0, x1) were written at least one
-// step earlier, so the DPP reads need no wait states.
+// One step, or two in one block.  On entry z holds this step's Z; a step
+// forms x0' and the next step's Z from kwn (the next step's x3 is this
+// step's x2, and its partner's x1 is the partner's present x0).  Written as
+// asm so that no instruction waits on the one before it, except the first
+// on the previous step's x0.  The DPP source (x0) was written at least one
+// step earlier (nine instructions), so the DPP read needs no wait states.
+#define KVGOV_LP_STEP(X0, X1, X2, Z, V, ZN, KWN, T1, T2, T3, XX, F, S)               \
+  "v_alignbit_b32 " T1 ", " X0 ", " X0 ", %[r1]\n\t"                              \
+  "v_alignbit_b32 " T2 ", " X0 ", " X0 ", %[r2]\n\t"                              \
+  "v_bitop3_b32 " XX ", " X0 ", " X1 ", %[m] bitop3:0xd2\n\t"                     \
+  "v_alignbit_b32 " T3 ", " X0 ", " X0 ", %[r3]\n\t"                              \
+  "v_bitop3_b32 " F ", " XX ", " X1 ", " X2 " bitop3:0xca\n\t"                    \
+  "v_bitop3_b32 " S ", " T1 ", " T2 ", " T3 " bitop3:0x96\n\t"                    \
+  "v_xad_u32 " ZN ", " X2 ", %[m], " KWN "\n\t"                                   \
+  "v_add3_u32 " V ", " S ", " F ", " Z "\n\t"                                     \
+  "v_add_u32_dpp " ZN ", " X0 ", " ZN " quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+
 __device__ __forceinline__ void lp_step(uint32_t s[4], uint32_t &z, uint32_t kwn,
                                         const LpLane &c) {
   uint32_t t1, t2, t3, x, f, sg, v, zn;
-  asm("v_alignbit_b32 %[t1], %[x0], %[x0], %[r1]\n\t"
-      "v_alignbit_b32 %[t2], %[x0], %[x0], %[r2]\n\t"
-      "v_bitop3_b32 %[x], %[x0], %[x1], %[m] bitop3:0xd2\n\t"
-      "v_alignbit_b32 %[t3], %[x0], %[x0], %[r3]\n\t"
-      "v_bitop3_b32 %[f], %[x], %[x1], %[x2] bitop3:0xca\n\t"
-      "v_bitop3_b32 %[sg], %[t1], %[t2], %[t3] bitop3:0x96\n\t"
-      "v_add_u32_dpp %[z], %[x0], %[z] row_ror:4 row_mask:0xf bank_mask:0xa\n\t"
-      "v_xad_u32 %[zn], %[x2], %[m], %[kwn]\n\t"
-      "v_add3_u32 %[v], %[sg], %[f], %[z]\n\t"
-      "v_add_u32_dpp %[zn], %[x1], %[zn] row_ror:12 row_mask:0xf bank_mask:0x5"
+  asm(KVGOV_LP_STEP("%[x0]", "%[x1]", "%[x2]", "%[z]", "%[v]", "%[zn]", "%[kwn]", "%[t1]",
+                    "%[t2]", "%[t3]", "%[x]", "%[f]", "%[sg]")
       : [t1] "=&v"(t1), [t2] "=&v"(t2), [x] "=&v"(x), [t3] "=&v"(t3), [f] "=&v"(f),
-        [sg] "=&v"(sg), [z] "+&v"(z), [zn] "=&v"(zn), [v] "=&v"(v)
-      : [x0] "v"(s[0]), [x1] "v"(s[1]), [x2] "v"(s[2]), [m] "v"(c.m), [r1] "v"(c.r1),
-        [r2] "v"(c.r2), [r3] "v"(c.r3), [kwn] "v"(kwn));
+        [sg] "=&v"(sg), [zn] "=&v"(zn), [v] "=&v"(v)
+      : [x0] "v"(s[0]), [x1] "v"(s[1]), [x2] "v"(s[2]), [z] "v"(z), [m] "v"(c.m),
+        [r1] "v"(c.r1), [r2] "v"(c.r2), [r3] "v"(c.r3), [kwn] "v"(kwn));
   s[3] = s[2];
   s[2] = s[1];
   s[1] = s[0];
   s[0] = v;
   z = zn;
+}
+
+__device__ __forceinline__ void lp_step2(uint32_t s[4], uint32_t &z, uint32_t kwn1,
+                                         uint32_t kwn2, const LpLane &c) {
+  uint32_t t1, t2, t3, x, f, sg, u1, u2, u3, y, g, sh, va, vb, za, zb;
+  asm(KVGOV_LP_STEP("%[x0]", "%[x1]", "%[x2]", "%[z]", "%[va]", "%[za]", "%[k1]", "%[t1]",
+                    "%[t2]", "%[t3]", "%[x]", "%[f]", "%[sg]")
+      KVGOV_LP_STEP("%[va]", "%[x0]", "%[x1]", "%[za]", "%[vb]", "%[zb]", "%[k2]", "%[u1]",
+                    "%[u2]", "%[u3]", "%[y]", "%[g]", "%[sh]")
+      : [t1] "=&v"(t1), [t2] "=&v"(t2), [x] "=&v"(x), [t3] "=&v"(t3), [f] "=&v"(f),
+        [sg] "=&v"(sg), [za] "=&v"(za), [va] "=&v"(va), [u1] "=&v"(u1), [u2] "=&v"(u2),
+        [y] "=&v"(y), [u3] "=&v"(u3), [g] "=&v"(g), [sh] "=&v"(sh), [zb] "=&v"(zb),
+        [vb] "=&v"(vb)
+      : [x0] "v"(s[0]), [x1] "v"(s[1]), [x2] "v"(s[2]), [z] "v"(z), [m] "v"(c.m),
+        [r1] "v"(c.r1), [r2] "v"(c.r2), [r3] "v"(c.r3), [k1] "v"(kwn1), [k2] "v"(kwn2));
+  s[3] = s[1];
+  s[2] = s[0];
+  s[1] = va;
+  s[0] = vb;
+  z = zb;
 }
 
 // N steps; kw holds the group's own kw (kw[0] is already in z), kw_after
@@ -693,24 +727,30 @@ template <int N>
 __device__ __forceinline__ void lp_steps(uint32_t s[4], uint32_t &z, const uint32_t *kw,
                                          uint32_t kw_after, const LpLane &c) {
 #pragma unroll
-  for (int i = 0; i < N; ++i) lp_step(s, z, i + 1 < N ? kw[i + 1] : kw_after, c);
+  for (int i = 0; i + 1 < N; i += 2)
+    lp_step2(s, z, kw[i + 1], i + 2 < N ? kw[i + 2] : kw_after, c);
+  if (N & 1) lp_step(s, z, kw_after, c);
 }
 
-// step 0 of a compression: the A lane's result is replaced by the initial a
-__device__ __forceinline__ void lp_first(uint32_t s[4], uint32_t &z, uint32_t kw1,
-                                         const LpLane &c, uint32_t a0, bool a_lane) {
+// steps 0 and 1 of a compression: the A lane's results are replaced by the
+// initial b, then a
+__device__ __forceinline__ void lp_head(uint32_t s[4], uint32_t &z, uint32_t kw1, uint32_t kw2,
+                                        const LpLane &c, uint32_t b0, uint32_t a0,
+                                        bool a_lane) {
   lp_step(s, z, kw1, c);
+  s[0] = a_lane ? b0 : s[0];
+  lp_step(s, z, kw2, c);
   s[0] = a_lane ? a0 : s[0];
 }
 
-// step 64: the A lane computes A_64; the E lane's words were final after
-// step 63 (e..h), the A lane's after step 64 (a..d)
-__device__ __forceinline__ void lp_last(uint32_t s[4], uint32_t &z, const LpLane &c,
+// steps 64 and 65: the A lane computes A_63 and A_64; the E lane's words
+// were final after step 63 (e..h), the A lane's after step 65 (a..d)
+__device__ __forceinline__ void lp_tail(uint32_t s[4], uint32_t &z, const LpLane &c,
                                         bool a_lane) {
   uint32_t e[4];
 #pragma unroll
   for (int x = 0; x < 4; ++x) e[x] = s[x];
-  lp_step(s, z, 1u, c);
+  lp_step2(s, z, 1u, 1u, c);
 #pragma unroll
   for (int x = 0; x < 4; ++x) s[x] = a_lane ? s[x] : e[x];
 }
@@ -734,21 +774,81 @@ __device__ __forceinline__ void lp_sched16(uint32_t w[16], uint32_t (*rows)[kLpC
   }
 }
 
-// K + W of block tokens Tn that depend on tokens only: C1 rounds 8..15 and
-// C2 rounds 0..7 and 16..63 (C2 rounds 8..15 are constants, set once)
-__device__ __forceinline__ void lp_prepare(const uint32_t Tn[16], LpLds &L, int buf, int lane) {
+// Per block and request, the three message patterns of the chain (the
+// compressions of a block, "first" and "second", plus a third for the
+// boundary block):
+//   plain        first (IV; h_{j-1} || T[0..7])   second (.; T[8..15] || pad96)
+//   first block  first (IV; T[0..15])             second (.; pad64)
+//   boundary     first (IV; sigma || h_{k-1})     second (.; T[0..15])
+//                third (.; pad128)
+// Prepared one block ahead from tokens and constants: the first message's
+// words into ha / hb except h_{j-1} (written by the rounds lanes at the end
+// of block j - 1), and K + W of all 64 rounds of the second message.
+__device__ __forceinline__ void lp_prepare(const uint32_t Tn[16], const uint32_t sig[8],
+                                           bool first_block, bool boundary, LpLds &L, int buf,
+                                           int lane) {
+  uint32_t m[16];
+  if (boundary) {
 #pragma unroll
-  for (int x = 0; x < 8; ++x) {
-    L.c1a[buf][x][lane] = kSha.K[8 + x] + Tn[x];
-    L.c2[buf][x][lane] = kSha.K[x] + Tn[8 + x];
+    for (int x = 0; x < 8; ++x) L.ha[x][lane] = sig[x];
+#pragma unroll
+    for (int x = 0; x < 16; ++x) m[x] = Tn[x];
+  } else if (first_block) {
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      L.ha[x][lane] = Tn[x];
+      L.hb[x][lane] = Tn[8 + x];
+    }
+    m[0] = 0x80000000u;
+#pragma unroll
+    for (int x = 1; x < 15; ++x) m[x] = 0;
+    m[15] = 64 * 8;
+  } else {
+#pragma unroll
+    for (int x = 0; x < 8; ++x) {
+      L.hb[x][lane] = Tn[x];
+      m[x] = Tn[8 + x];
+    }
+    pad96_tail(m);
   }
-  uint32_t w[16];
 #pragma unroll
-  for (int x = 0; x < 8; ++x) w[x] = Tn[8 + x];
-  pad96_tail(w);
-  lp_sched16<16>(w, L.c2[buf], 16, lane);
-  lp_sched16<32>(w, L.c2[buf], 32, lane);
-  lp_sched16<48>(w, L.c2[buf], 48, lane);
+  for (int x = 0; x < 16; ++x) L.c2[buf][x][lane] = kSha.K[x] + m[x];
+  lp_sched16<16>(m, L.c2[buf], 16, lane);
+  lp_sched16<32>(m, L.c2[buf], 32, lane);
+  lp_sched16<48>(m, L.c2[buf], 48, lane);
+}
+
+__device__ __forceinline__ void lp_load16(uint32_t w[16], const uint32_t (*rows)[2], int base,
+                                          int col) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) w[i] = rows[base + i][col];
+}
+
+// The rounds of one compression from the initial words st (E: e..h, A:
+// a..d), K + W from 16-row groups: kw0 holds rounds 0..15 (already in
+// registers), the later groups are loaded from `rows` (64 rows) one group
+// ahead; returns st + the compression's result.
+template <typename Rows>
+__device__ __forceinline__ void lp_compress_rows(uint32_t st[4], const uint32_t kw0[16], Rows rows,
+                                                 int col, const LpLane &c, bool a_lane) {
+  uint32_t s[4], wa[16], wb[16], z;
+#pragma unroll
+  for (int x = 0; x < 4; ++x) s[x] = a_lane ? (x < 2 ? st[x + 2] : 0u) : st[x];
+  z = lp_z0(s, kw0[0], c);
+  lp_load16(wa, rows, 16, col);
+  __builtin_amdgcn_sched_barrier(0);
+  lp_head(s, z, kw0[1], kw0[2], c, st[1], st[0], a_lane);
+  lp_steps<14>(s, z, kw0 + 2, wa[0], c);   // 2..15
+  lp_load16(wb, rows, 32, col);
+  __builtin_amdgcn_sched_barrier(0);
+  lp_steps<16>(s, z, wa, wb[0], c);        // 16..31
+  lp_load16(wa, rows, 48, col);
+  __builtin_amdgcn_sched_barrier(0);
+  lp_steps<16>(s, z, wb, wa[0], c);        // 32..47
+  lp_steps<16>(s, z, wa, 1u, c);           // 48..63
+  lp_tail(s, z, c, a_lane);
+#pragma unroll
+  for (int x = 0; x < 4; ++x) st[x] += s[x];
 }
 
 // Workgroup `group` of the lane-pair kernel: requests group * 64 + 0..63 of
@@ -760,11 +860,9 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
   const int wave = threadIdx.x / kWave;
   const bool sched_wave = wave >= 2;
   const bool idle = wave >= 3;
-  const bool a_lane = !sched_wave && ((lane >> 2) & 1);
-  const int pos = lane & 15;
+  const bool a_lane = !sched_wave && (lane & 1);
   // the request (LDS column) of this lane within the workgroup
-  const int mine =
-      sched_wave ? lane : wave * 32 + (lane >> 4) * 8 + ((pos >> 3) << 2) + (pos & 3);
+  const int mine = sched_wave ? lane : wave * 32 + (lane >> 1);
   const int32_t base = group * kWave;
   const int32_t i = base + mine;
 
@@ -775,11 +873,12 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
     ok = chain_setup<MODE>(a, r, q);
   }
   const int64_t nf = ok ? q.nf : 0;
-  // Trip count and special iterations are decided over all 64 requests of
+  const int64_t kb = ok ? q.k : -1;  // boundary block (boundary mode), else -1
+  // Trip count and boundary iterations are decided over all 64 requests of
   // the workgroup: the schedule wave holds them all, and a rounds lane also
   // looks at the request of the same lane in the other rounds wave.
-  const ReqPeek own{nf, ok ? q.k : -1, ok && !q.salted_root};
-  ReqPeek other{0, -1, false};
+  const ReqPeek own{nf, kb};
+  ReqPeek other{0, -1};
   if (!sched_wave) other = req_peek<MODE>(a, base + (1 - wave) * 32 + (mine & 31));
   int64_t J = own.nf > other.nf ? own.nf : other.nf;
 #pragma unroll
@@ -787,20 +886,14 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
     const int64_t o = __shfl_xor(J, d, kWave);
     J = o > J ? o : J;
   }
-  const bool plain_first = ok && !q.salted_root;
 
-  // constant column of every table; constant rows 8..15 of C2 (padding)
+  // constant columns; the padding block of a 128-byte message
   uint32_t(*rows)[kLpCols] = reinterpret_cast<uint32_t(*)[kLpCols]>(&L);
   for (int x = threadIdx.x; x < kLpRows; x += blockDim.x)
-    rows[x][kWave] = x < 8 ? 1u - kShaDev.K[x] : 1u;
-  if (sched_wave && !idle) {
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      L.c2[b][8][lane] = kSha.K[8] + 0x80000000u;
-#pragma unroll
-      for (int x = 9; x < 15; ++x) L.c2[b][x][lane] = kSha.K[x];
-      L.c2[b][15][lane] = kSha.K[15] + 96 * 8;
-    }
+    rows[x][kWave] = x < 16 ? 1u - kShaDev.K[x] : 1u;
+  for (int x = threadIdx.x; x < 64; x += blockDim.x) {
+    L.c3[x][0] = kPad128Dev.kw[x];
+    L.c3[x][1] = 1u;
   }
 
   // rounds lanes: role constants
@@ -810,26 +903,30 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
   c.r3 = a_lane ? 22 : 25;
   c.m = a_lane ? ~0u : 0u;
   const int col = a_lane ? kWave : mine;
+  const int col3 = a_lane ? 1 : 0;
   const int half = a_lane ? 0 : 4;  // state words held: a..d = 0..3, e..h = 4..7
-  uint32_t iv[4];  // the initial value's words held by the lane
+  uint32_t iv[4];                   // the initial value's words held by the lane
 #pragma unroll
   for (int x = 0; x < 4; ++x) iv[x] = a_lane ? kSha.H0[x] : kSha.H0[4 + x];
-  uint32_t iv0[4];  // step-0 registers of the first compression (A: b, c, d, -)
-#pragma unroll
-  for (int x = 0; x < 4; ++x) iv0[x] = a_lane ? (x < 3 ? kSha.H0[x + 1] : 0u) : kSha.H0[4 + x];
 
-  u32x4 nxt[4];  // schedule wave: tokens of the next block
-  if (sched_wave) {
-    if (nf > 0 && !idle) {
-      load_raw(q.tp, nxt);
-      uint32_t T0[16];
-      swap_block(nxt, T0);
-      lp_prepare(T0, L, 0, lane);
-    }
-  } else if (!a_lane && ok) {
-    // h_{-1}: sigma for a root-salted first block, else unused
+  // schedule wave: tokens one block ahead (lanes without blocks read a
+  // valid dummy block: the loop runs only if some request of the workgroup
+  // has a block, so the token array holds at least 16 tokens)
+  u32x4 nxt[4];
+  const int32_t *tp = nf > 0 ? q.tp : a.tokens;
+  const int64_t nfl = nf > 0 ? nf : 1;
+  if (sched_wave && !idle && J > 0) {
+    load_raw(tp, nxt);
+    uint32_t T0[16];
+    take_block(nxt, T0, tp, 0, nfl);
+    if (nf > 0) {
+      const bool salted = q.salted_root;
+      if (salted) {
 #pragma unroll
-    for (int w = 0; w < 8; ++w) L.h[w][mine] = q.salted_root ? q.sig[w] : 0u;
+        for (int x = 0; x < 8; ++x) L.ha[x][lane] = q.sig[x];  // h_{-1} = sigma
+      }
+      lp_prepare(T0, q.sig, !salted, false, L, 0, lane);
+    }
   }
   __syncthreads();
 
@@ -837,105 +934,82 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
     const bool act = j < nf;
     const bool next = j + 1 < nf;
     const int cb = (int)(j & 1), nb = cb ^ 1;
-    uint32_t T[16];  // schedule wave: tokens of block j
-    if (sched_wave && act && !idle) take_block(nxt, T, q.tp, j, nf);
-
-    bool special_any = false;
-    if (MODE != KVGOV_ROOT)
-      special_any = req_special<MODE>(own, j) || req_special<MODE>(other, j);
-    if (MODE != KVGOV_ROOT && __any(special_any)) {
-      // special iteration: the E lane of every request does its whole block
-      if (sched_wave) {
-        if (next && !idle) {
-          uint32_t Tn[16];
-          swap_block(nxt, Tn);
-          lp_prepare(Tn, L, nb, lane);
-        }
-      } else if (act && !a_lane) {
-        const bool u0 = plain_first && j == 0;
-        const bool bnd = (MODE == KVGOV_BOUNDARY) && j == q.k && q.k > 0;
-        u32x4 raw[4];
-        uint32_t H[8], Tb[16];
-        load_raw(q.tp + 16 * j, raw);
-        swap_block(raw, Tb);
-#pragma unroll
-        for (int w = 0; w < 8; ++w) H[w] = L.h[w][mine];
-        special_block(H, Tb, q.sig, u0, bnd);
-#pragma unroll
-        for (int w = 0; w < 8; ++w) L.h[w][mine] = H[w];
-        store_digest(q.out + j * 32, H);
-      }
-      __syncthreads();
-      continue;
+    // boundary blocks take a third compression (workgroup-uniform decision)
+    bool third = false;
+    if (MODE == KVGOV_BOUNDARY) {
+      const bool mine_bnd = (j < own.nf && j == own.k && own.k > 0) ||
+                            (j < other.nf && j == other.k && other.k > 0);
+      third = __any(mine_bnd);
     }
 
     if (!sched_wave) {
       // ---- rounds waves.  Step i of a group takes the kw of step i + 1 (the
-      // next step's z starts early).
+      // next step's z starts early).  Each barrier comes C steps before the
+      // first word it releases is taken, so that the LDS reads after it are
+      // covered by those steps.
+      constexpr int C = KVGOV_LP_COVER;
       uint32_t s[4], st[4], wa[16], wb[16], z = 0;
+      uint32_t kw16[16];
       if (act) {
-        uint32_t kw8[8];
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-          kw8[t] = kSha.K[t] + L.h[t][col];
-          wa[8 + t] = L.c1a[cb][t][col];
+          kw16[t] = kSha.K[t] + L.ha[t][col];
+          kw16[8 + t] = kSha.K[8 + t] + L.hb[t][col];
         }
 #pragma unroll
-        for (int x = 0; x < 4; ++x) s[x] = iv0[x];
-        z = lp_z0(s, kw8[0], c);
-        lp_first(s, z, kw8[1], c, kSha.H0[0], a_lane);
-        lp_steps<7>(s, z, kw8 + 1, wa[8], c);    // rounds 1..7
-        lp_steps<4>(s, z, wa + 8, wa[12], c);    // 8..11
+        for (int x = 0; x < 4; ++x) s[x] = a_lane ? (x < 2 ? iv[x + 2] : 0u) : iv[x];
+        z = lp_z0(s, kw16[0], c);
+        lp_head(s, z, kw16[1], kw16[2], c, iv[1], iv[0], a_lane);
+        lp_steps<6>(s, z, kw16 + 2, kw16[8], c);  // steps 2..7
+        lp_steps<8 - C>(s, z, kw16 + 8, kw16[16 - C], c);
       }
-      __syncthreads();  // C1 rounds 16..31 ready
+      __syncthreads();  // first compression, rounds 16..31 ready
       if (act) {
         lp_load16(wb, L.c1b, 0, col);
         __builtin_amdgcn_sched_barrier(0);
-        lp_steps<4>(s, z, wa + 12, wb[0], c);    // 12..15
-        lp_steps<12>(s, z, wb, wb[12], c);       // 16..27
+        lp_steps<C>(s, z, kw16 + 16 - C, wb[0], c);
+        lp_steps<16 - C>(s, z, wb, wb[16 - C], c);  // from 16
       }
-      __syncthreads();  // C1 rounds 32..47 ready
+      __syncthreads();  // rounds 32..47 ready
       if (act) {
         lp_load16(wa, L.c1b, 16, col);
         __builtin_amdgcn_sched_barrier(0);
-        lp_steps<4>(s, z, wb + 12, wa[0], c);    // 28..31
-        lp_steps<12>(s, z, wa, wa[12], c);       // 32..43
+        lp_steps<C>(s, z, wb + 16 - C, wa[0], c);
+        lp_steps<16 - C>(s, z, wa, wa[16 - C], c);  // from 32
       }
-      __syncthreads();  // C1 rounds 48..63 ready
+      __syncthreads();  // rounds 48..63 ready
       if (act) {
         lp_load16(wb, L.c1b, 32, col);
         __builtin_amdgcn_sched_barrier(0);
-        lp_steps<4>(s, z, wa + 12, wb[0], c);    // 44..47
+        lp_steps<C>(s, z, wa + 16 - C, wb[0], c);
         lp_load16(wa, L.c2[cb], 0, col);
         __builtin_amdgcn_sched_barrier(0);
-        lp_steps<16>(s, z, wb, 1u, c);           // 48..63
-        lp_last(s, z, c, a_lane);
+        lp_steps<16>(s, z, wb, 1u, c);  // 48..63
+        lp_tail(s, z, c, a_lane);
 #pragma unroll
         for (int x = 0; x < 4; ++x) st[x] = iv[x] + s[x];
-        // C2 step-0 registers: E: e, f, g, h; A: b, c, d, -
+        // second compression
+        lp_compress_rows(st, wa, L.c2[cb], col, c, a_lane);
+        if (MODE == KVGOV_BOUNDARY && third) {
+          // third compression (the boundary block's padding), for all lanes;
+          // only boundary requests keep its result
+          uint32_t st3[4], k3[16];
 #pragma unroll
-        for (int x = 0; x < 4; ++x) s[x] = a_lane ? (x < 3 ? st[x + 1] : 0u) : st[x];
-        z = lp_z0(s, wa[0], c);
-        lp_load16(wb, L.c2[cb], 16, col);
-        __builtin_amdgcn_sched_barrier(0);
-        lp_first(s, z, wa[1], c, st[0], a_lane);
-        lp_steps<15>(s, z, wa + 1, wb[0], c);    // C2 1..15
-        lp_load16(wa, L.c2[cb], 32, col);
-        __builtin_amdgcn_sched_barrier(0);
-        lp_steps<16>(s, z, wb, wa[0], c);        // 16..31
-        lp_load16(wb, L.c2[cb], 48, col);
-        __builtin_amdgcn_sched_barrier(0);
-        lp_steps<16>(s, z, wa, wb[0], c);        // 32..47
-        lp_steps<16>(s, z, wb, 1u, c);           // 48..63
-        lp_last(s, z, c, a_lane);
-        uint32_t o[4];
+          for (int x = 0; x < 4; ++x) st3[x] = st[x];
+          lp_load16(k3, L.c3, 0, col3);
+          lp_compress_rows(st3, k3, L.c3, col3, c, a_lane);
+          const bool bnd = j == kb && kb > 0;
 #pragma unroll
-        for (int x = 0; x < 4; ++x) {
-          o[x] = st[x] + s[x];
-          L.h[half + x][mine] = o[x];
+          for (int x = 0; x < 4; ++x) st[x] = bnd ? st3[x] : st[x];
         }
+        // h_j: the next block's first message words 0..7 (plain), or 8..15
+        // (the next block is the boundary block)
+        const bool next_bnd = MODE == KVGOV_BOUNDARY && kb > 0 && j + 1 == kb;
+        uint32_t(*hrows)[kLpCols] = next_bnd ? L.hb : L.ha;
+#pragma unroll
+        for (int x = 0; x < 4; ++x) hrows[half + x][mine] = st[x];
         u32x4 *dst = reinterpret_cast<u32x4 *>(q.out + j * 32 + half * 4);
-        *dst = u32x4{bswap(o[0]), bswap(o[1]), bswap(o[2]), bswap(o[3])};
+        *dst = u32x4{bswap(st[0]), bswap(st[1]), bswap(st[2]), bswap(st[3])};
       }
       __syncthreads();
     } else {
@@ -944,8 +1018,8 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
       if (act && !idle) {
 #pragma unroll
         for (int x = 0; x < 8; ++x) {
-          w[x] = L.h[x][lane];
-          w[8 + x] = T[x];
+          w[x] = L.ha[x][lane];
+          w[8 + x] = L.hb[x][lane];
         }
         lp_sched16<16>(w, L.c1b, 0, lane);
       }
@@ -954,10 +1028,15 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
       __syncthreads();
       if (act && !idle) lp_sched16<48>(w, L.c1b, 32, lane);
       __syncthreads();
-      if (next && !idle) {
+      if (!idle) {
+        // block j + 1's tokens, and the load of block j + 2
         uint32_t Tn[16];
-        swap_block(nxt, Tn);
-        lp_prepare(Tn, L, nb, lane);
+        const int64_t jn = j + 1 < nfl ? j + 1 : nfl - 1;
+        take_block(nxt, Tn, tp, jn, nfl);
+        if (next) {
+          const bool bnd_next = MODE == KVGOV_BOUNDARY && kb > 0 && j + 1 == kb;
+          lp_prepare(Tn, q.sig, false, bnd_next, L, nb, lane);
+        }
       }
       __syncthreads();
     }
