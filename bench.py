@@ -521,8 +521,11 @@ def main():
     look_bytes = {m: lookup_bytes(B, got_hits[m]) for m in modes}
     look_mean = {m: float(np.mean(ts)) for m, ts in look_t.items()}
     look_gbs = float(np.mean([look_bytes[m] / look_mean[m] for m in modes])) / 1e9
-    g_look = 1  # lanes per request the library picks for this batch size
+    g_look = 1  # lanes per request the library picks for this batch
     while g_look < 64 and B.n * g_look * 2 <= (1 << 18):
+        g_look <<= 1
+    avg_blocks = int(B.block_counts().sum()) // max(B.n, 1)
+    while g_look < 64 and g_look * 16 <= avg_blocks and B.n * g_look * 2 <= (1 << 21):
         g_look <<= 1
     ltr = recorded_traffic(f"k_lookup<{g_look}>", wl.name, "cache")
     roof_lookup = {

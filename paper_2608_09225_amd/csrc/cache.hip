@@ -134,6 +134,69 @@ __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t *lds4) {
 // Tags only ever change from 0 to a claim, so a plain (possibly stale) read
 // can only show 0 for a claimed slot; the compare-and-swap that follows then
 // fails and returns the claim.  Coherent atomics are used for the claim only.
+// Returns 1 if the key was added.
+__device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &key, int64_t i,
+                                               int64_t lo, const uint8_t *hashes,
+                                               uint32_t epoch) {
+  if (key_is_empty_pattern(key)) return atomicExch(&t.meta->ones_present, 1) == 0 ? 1u : 0u;
+  const unsigned long long mine = ((unsigned long long)epoch << 32) |
+                                  (unsigned long long)(i - lo + 1);
+  uint64_t s = slot_hash(key) & t.mask;
+  for (uint64_t probes = 0; probes <= t.mask; ++probes) {
+    unsigned long long tag = t.tags[s];
+    if (tag == 0) {
+      unsigned long long expect = 0;
+      if (__hip_atomic_compare_exchange_strong(&t.tags[s], &expect, mine, __ATOMIC_RELAXED,
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+        t.keys[2 * s] = key.lo;
+        t.keys[2 * s + 1] = key.hi;
+        return 1;
+      }
+      tag = expect;  // somebody claimed it first: examine the claimant
+    }
+    Key other;
+    if ((uint32_t)(tag >> 32) == epoch) {
+      const int64_t c = (int64_t)(tag & 0xFFFFFFFFull) - 1;
+      other = load_key(hashes + (lo + c) * 32);
+    } else {
+      other = Key{t.keys[2 * s], t.keys[2 * s + 1]};
+    }
+    if (key_eq(key, other)) return 0;
+    s = (s + 1) & t.mask;
+  }
+  atomicCAS(&t.meta->status, 0, KVGOV_E_FULL);
+  return 0;
+}
+
+// Consecutive keys per wave chunk of the insert.
+constexpr int kInsChunk = 128;
+
+// The largest r in [0, n) with bo[r] <= f (bo non-decreasing in a valid
+// batch; any answer in range is harmless otherwise, see k_insert).  Every
+// lane of a wave searches the same f.
+__device__ __forceinline__ int32_t find_request(const int64_t *bo, int32_t n, int64_t f) {
+  int32_t a = 0, b = n - 1;
+  while (a < b) {
+    const int32_t mid = (a + b + 1) >> 1;
+    if (bo[mid] <= f) a = mid; else b = mid - 1;
+  }
+  return a;
+}
+
+// Batched insert.  A wave takes chunks of kInsChunk consecutive keys, 64 at
+// a time.  Before touching the table a key is compared with the key at the
+// same block position of the previous request (requests that share a prefix
+// - the same principal, or any principal below the boundary block - hold
+// the same keys there): an equal earlier key makes this one a duplicate
+// that needs no table access, so a prefix shared by thousands of requests
+// costs a few table operations per key instead of thousands of atomics on
+// one slot.  The request of each key comes from a window of 64 request
+// starts (a search over lanes); the comparison is only an optimisation:
+// skipping a key that equals an earlier key of the batch is always correct
+// (the earlier one is inserted, or is itself a duplicate of an earlier
+// one), and the compared position is checked to lie in the batch, so
+// malformed interior offsets cannot cause a wrong result or an
+// out-of-range read.
 __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hashes,
                                                 const int64_t *blk_offsets, int32_t n,
                                                 int64_t n_blocks, uint32_t epoch) {
@@ -146,53 +209,46 @@ __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hash
     if (first) atomicCAS(&t.meta->status, 0, KVGOV_E_OFFSETS);
     return;
   }
-  const int64_t stride = (int64_t)gridDim.x * 256;
-  const uint64_t slots = t.mask + 1;
+  const int lane = threadIdx.x & 63;
+  const int64_t waves = (int64_t)gridDim.x * 4;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   uint32_t added = 0;
-  for (int64_t i = lo + (int64_t)blockIdx.x * 256 + threadIdx.x; i < hi; i += stride) {
-    const Key key = load_key(hashes + i * 32);
-    if (key_is_empty_pattern(key)) {
-      if (atomicExch(&t.meta->ones_present, 1) == 0) ++added;
-      continue;
-    }
-    const unsigned long long mine =
-        ((unsigned long long)epoch << 32) | (unsigned long long)(i - lo + 1);
-    uint64_t s = slot_hash(key) & t.mask;
-    uint64_t probes = 0;
-    while (true) {
-      unsigned long long tag = t.tags[s];
-      if (tag == 0) {
-        unsigned long long expect = 0;
-        if (__hip_atomic_compare_exchange_strong(&t.tags[s], &expect, mine, __ATOMIC_RELAXED,
-                                                 __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT)) {
-          t.keys[2 * s] = key.lo;
-          t.keys[2 * s + 1] = key.hi;
-          ++added;
-          break;
-        }
-        tag = expect;  // somebody claimed it first: examine the claimant
+  for (int64_t f0 = lo + wave * kInsChunk; f0 < hi; f0 += waves * kInsChunk) {
+    const int64_t f1 = f0 + kInsChunk < hi ? f0 + kInsChunk : hi;
+    int32_t rc = find_request(blk_offsets, n, f0);
+    for (int64_t fb = f0; fb < f1; fb += 64) {
+      // win[l] = start of request rc - 1 + l (clamped to [0, n])
+      int32_t wi = rc - 1 + lane;
+      wi = wi < 0 ? 0 : (wi > n ? n : wi);
+      const int64_t win = blk_offsets[wi];
+      const int64_t f = fb + lane;
+      // pos: the largest l in [1, 63] with win[l] <= f
+      int pos = 1;
+#pragma unroll
+      for (int step = 32; step >= 1; step >>= 1) {
+        const int cand = pos + step;
+        const int64_t v = __shfl(win, cand < 63 ? cand : 63, 64);
+        if (cand <= 63 && v <= f) pos = cand;
       }
-      Key other;
-      if ((uint32_t)(tag >> 32) == epoch) {
-        const int64_t c = (int64_t)(tag & 0xFFFFFFFFull) - 1;
-        other = load_key(hashes + (lo + c) * 32);
-      } else {
-        other = Key{t.keys[2 * s], t.keys[2 * s + 1]};
+      const int64_t b_r = __shfl(win, pos, 64);
+      const int64_t b_p = __shfl(win, pos - 1, 64);
+      const int32_t r = rc - 1 + pos;
+      if (f < f1) {
+        const Key key = load_key(hashes + f * 32);
+        bool dup = false;
+        const int64_t jj = f - b_r;
+        if (r >= 1 && jj >= 0 && jj < b_r - b_p && b_p + jj >= lo)
+          dup = key_eq(key, load_key(hashes + (b_p + jj) * 32));
+        if (!dup) added += insert_key(t, key, f, lo, hashes, epoch);
       }
-      if (key_eq(key, other)) break;
-      s = (s + 1) & t.mask;
-      if (++probes >= slots) {
-        atomicCAS(&t.meta->status, 0, KVGOV_E_FULL);
-        break;
-      }
+      rc = __shfl(r, 63, 64);
     }
   }
   const uint32_t total = block_sum(added, lds4);
   if (threadIdx.x == 0 && total) {
-    const int lane = blockIdx.x % kCounterLanes;
-    atomicAdd(&t.meta->new_keys[epoch & 1][lane], (unsigned long long)total);
-    atomicAdd(&t.meta->n_keys[lane], (unsigned long long)total);
+    const int cl = blockIdx.x % kCounterLanes;
+    atomicAdd(&t.meta->new_keys[epoch & 1][cl], (unsigned long long)total);
+    atomicAdd(&t.meta->n_keys[cl], (unsigned long long)total);
   }
 }
 
@@ -439,7 +495,10 @@ int kvgov_cache_insert(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
   hipStream_t s = as_stream(stream);
   uint32_t epoch = c->epoch.fetch_add(1) + 1;
   if (epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;  // 2^32 - 1 inserts since clear
-  hipLaunchKernelGGL(k_insert, dim3(grid_for(n_blocks, 32)), dim3(256), 0, s, c->view, hashes,
+  const int64_t ins_groups = ceil_div(std::max<int64_t>(n_blocks, 1), (int64_t)kInsChunk * 4);
+  const unsigned ins_grid =
+      (unsigned)std::min<int64_t>(ins_groups, (int64_t)device_cu_count() * 16);
+  hipLaunchKernelGGL(k_insert, dim3(ins_grid), dim3(256), 0, s, c->view, hashes,
                      blk_offsets, n, n_blocks, epoch);
   rc = launch_status();
   if (rc != KVGOV_OK || !n_new) return rc;
@@ -453,10 +512,16 @@ int kvgov_cache_insert(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
 }
 
 // Lanes per request for lookup: enough groups in flight to cover the chip
-// (about 2^18 lanes), one lane each when the batch alone is that large.
-static int lookup_group(int32_t n) {
+// (about 2^18 lanes), one lane each when the batch alone is that large; and,
+// up to about 2^21 lanes, one lane per ~16 blocks of the average request,
+// since a group walks its request's blocks G at a time and the longest
+// request bounds the launch (a batch of long requests would otherwise wait on
+// its longest one with one or two lanes).
+static int lookup_group(int32_t n, int64_t n_blocks) {
   int g = 1;
   while (g < 64 && (int64_t)n * g * 2 <= (1 << 18)) g <<= 1;
+  const int64_t avg = n > 0 ? n_blocks / n : 0;
+  while (g < 64 && (int64_t)g * 16 <= avg && (int64_t)n * g * 2 <= (1 << 21)) g <<= 1;
   return g;
 }
 
@@ -471,7 +536,7 @@ int kvgov_cache_lookup(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
   if (n == 0) return KVGOV_OK;
   hipStream_t s = as_stream(stream);
   LookupArgs a{c->view, hashes, blk_offsets, n, n_blocks, hit_blocks};
-  const int g = lookup_group(n);
+  const int g = lookup_group(n, n_blocks);
   const dim3 grid((unsigned)ceil_div((int64_t)n * g, 256)), block(256);
   switch (g) {
     case 1: hipLaunchKernelGGL(k_lookup<1>, grid, block, 0, s, a); break;
