@@ -316,11 +316,63 @@ def test_cache_bad_offsets_latched():
             c.count()
 
 
-@pytest.mark.parametrize("n_req", [1, 7, 64, 5000, 300000])
+def test_cache_insert_shared_prefixes():
+    """Requests sharing prefixes with their neighbours (the insert skips keys
+    equal to the previous request's key at the same position), runs of empty
+    and one-block requests, and duplicates far apart: the table receives
+    exactly the batch's key set."""
+    g = np.random.default_rng(111)
+    fam = g.integers(0, 256, (12, 300, 32), dtype=np.uint8)
+    lens, rows = [], []
+    for r in range(4000):
+        kind = r % 10
+        if kind == 0:
+            L = 0
+        elif kind in (1, 2):
+            L = 1
+        else:
+            L = int(g.integers(1, 250))
+        f = (r // 7) % 12 if kind < 8 else int(g.integers(0, 12))  # runs, then random
+        s = int(g.integers(0, L + 1))
+        k = g.integers(0, 256, (L, 32), dtype=np.uint8)
+        k[:s] = fam[f, :s]
+        lens.append(L)
+        rows.append(k)
+    # a long run of one-block requests with identical keys (window overflow)
+    for r in range(300):
+        lens.append(1)
+        rows.append(fam[0, :1].copy())
+    keys = np.concatenate(rows)
+    bo = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    want = key_set(keys)
+    with K.Cache(20) as c:
+        assert c.insert(dev(keys), dev(bo)) == len(want)
+        assert c.count() == len(want)
+        assert key_set(c.export().cpu().numpy()) == want
+        assert c.insert(dev(keys), dev(bo)) == 0
+        hits = c.lookup(dev(keys), dev(bo)).cpu().numpy()
+    assert np.array_equal(hits, np.asarray(lens))
+
+
+def test_cache_insert_ignores_interior_offsets():
+    """Insert adds the flat range [blk_offsets[0], blk_offsets[n]); interior
+    offsets that are not monotone change nothing."""
+    g = np.random.default_rng(121)
+    uniq = g.integers(0, 256, (500, 32), dtype=np.uint8)
+    keys = uniq[g.integers(0, 500, 9000)]
+    keys[4000:4500] = keys[3000:3500]  # a repeated stretch
+    bo = np.array([0, 5000, 100, 7000, 20, 8999, 3, 9000], np.int64)
+    with K.Cache(12) as c:
+        assert c.insert(dev(keys), dev(bo)) == len(key_set(keys))
+        assert key_set(c.export().cpu().numpy()) == key_set(keys)
+
+
+@pytest.mark.parametrize("n_req", [1, 7, 64, 5000, 20000, 300000])
 def test_cache_lookup_group_sizes(n_req):
     """Lookups at batch sizes that select every lanes-per-request width."""
     g = np.random.default_rng(n_req)
-    nb = g.integers(0, 70, n_req).astype(np.int64)
+    # long requests at 20000 (lanes per request from the average length)
+    nb = g.integers(0, 400 if n_req == 20000 else 70, n_req).astype(np.int64)
     bo = np.concatenate([[0], np.cumsum(nb)])
     keys = g.integers(0, 256, (int(bo[-1]), 32), dtype=np.uint8)
     # insert a random prefix of each request's keys
