@@ -326,6 +326,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="paper", choices=sorted(DESCRIPTIONS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the critical-path launch and the measured-peak "
+                         "microbenchmarks (counter runs: only the step's own launches)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before the bench, run one device-to-device copy of this many MiB "
                          "(a kernel of known traffic, to scale HBM byte counters)")
@@ -650,6 +653,7 @@ def main():
             "bytes_note": f"{INSERT_BYTES_NEW} B per new key (query read, slot read, slot "
                           f"write), {INSERT_BYTES_PRESENT} B per present key",
         }
+    if not probe_only and not args.no_extras:
         # Critical path: the per-block latency of the lane-pair kernel under a
         # realistic load (the longest request replicated into one 64-request
         # workgroup per CU; a single workgroup on an otherwise idle GPU runs
@@ -688,16 +692,17 @@ def main():
                                       "(launch ops at peak) / its duration")
         del o, oh
 
-    log("measuring device peaks (microbenchmarks)")
-    mp = measured_peaks(dev)
-    result["measured_peaks"] = mp
-    roof = result["roofline"]
-    if roof["bound"] == "alu":
-        roof["frac_of_measured_peak"] = roof["achieved"] / mp["int_valu_tops"]
-    for key in ("roofline_lookup", "roofline_insert", "roofline"):
-        rr = result.get(key)
-        if rr and rr["bound"] == "hbm":
-            rr["frac_of_measured_gather32"] = rr["achieved"] / mp["gather32_gbs"]
+    if not args.no_extras:
+        log("measuring device peaks (microbenchmarks)")
+        mp = measured_peaks(dev)
+        result["measured_peaks"] = mp
+        roof = result["roofline"]
+        if roof["bound"] == "alu":
+            roof["frac_of_measured_peak"] = roof["achieved"] / mp["int_valu_tops"]
+        for key in ("roofline_lookup", "roofline_insert", "roofline"):
+            rr = result.get(key)
+            if rr and rr["bound"] == "hbm":
+                rr["frac_of_measured_gather32"] = rr["achieved"] / mp["gather32_gbs"]
 
     h = args.steps // 2
     a1, a2 = np.mean(per_step[:h]), np.mean(per_step[h:])
