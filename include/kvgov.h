@@ -35,7 +35,8 @@
  *   - K and the salts are secrets: the library keeps no copy of K after
  *     kvgov_salts returns and logs nothing.
  *   - The calls allocate no device memory except kvgov_cache_create and the
- *     stream-ordered scratch of kvgov_hash_chains (see there).
+ *     stream-ordered scratch of kvgov_hash_chains and its resume variant
+ *     (see there) and of the offset helpers (8 bytes per 1024 requests).
  */
 #ifndef KVGOV_H
 #define KVGOV_H
@@ -144,6 +145,49 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens,
                       int32_t mode, const int32_t *boundary_tok, int32_t block_size,
                       const int64_t *blk_offsets, uint8_t *hashes, int64_t n_blocks,
                       int32_t *status, void *stream);
+
+/*
+ * Chain extension (Sec. 2.1; Sec. 5.7 on multi-turn sessions, where turn
+ * n+1 extends turn n exactly).  Because h_j depends only on h_{j-1}, T_j and,
+ * for the salted block, sigma_p, a chain whose digests up to block j0 - 1 are
+ * already known resumes at block j0 from h_{j0-1}: the result is exactly rows
+ * j0 .. len_r/16 - 1 of what kvgov_hash_chains computes for the whole
+ * request.  The prefix is neither read nor rehashed.
+ *
+ * Arguments as for kvgov_hash_chains (tokens hold each request's whole
+ * sequence; only the tokens of blocks >= j0 are read; boundary_tok is the
+ * whole sequence's), plus:
+ * start_block  device, int32 [n]: j0 of request r, in [0, len_r / 16]
+ *              (outside: KVGOV_E_OFFSETS in `status`, request skipped).
+ *              j0 = 0 hashes the whole chain; j0 = len_r / 16 hashes nothing.
+ * parents      device, uint8 [n][32], 4-byte aligned: h_{j0-1} of request r,
+ *              read only when j0 > 0 (the row's content is then trusted; the
+ *              salt, root or boundary, is already inside it when j0 is past
+ *              the salted block).
+ * blk_offsets  device, int64 [n + 1]: exclusive prefix sum of
+ *              len_r / 16 - j0 (kvgov_resume_offsets); request r's block
+ *              j0 + i goes to row blk_offsets[r] + i.
+ * Errors: as kvgov_hash_chains; KVGOV_E_INVAL also for NULL start_block or
+ * parents with n > 0, or misaligned parents.
+ */
+int kvgov_hash_chains_resume(const int32_t *tokens, int64_t n_tokens,
+                             const int64_t *tok_offsets, int32_t n,
+                             const int32_t *principal, const uint8_t *salts, int32_t P,
+                             int32_t mode, const int32_t *boundary_tok, int32_t block_size,
+                             const int32_t *start_block, const uint8_t *parents,
+                             const int64_t *blk_offsets, uint8_t *hashes, int64_t n_blocks,
+                             int32_t *status, void *stream);
+
+/*
+ * Output layout of kvgov_hash_chains_resume: blk_offsets[r] =
+ * sum_{i<r} (floor(len_i / 16) - start_block[i]); blk_offsets[0] = 0.
+ * A negative length or a start block outside [0, len_i / 16] stores
+ * KVGOV_E_OFFSETS in `status` and counts as 0 blocks.  Otherwise as
+ * kvgov_block_offsets; KVGOV_E_INVAL for NULL start_block with n > 0.
+ */
+int kvgov_resume_offsets(const int64_t *tok_offsets, const int32_t *start_block, int32_t n,
+                         int32_t block_size, int64_t *blk_offsets, int32_t *status,
+                         void *stream);
 
 /*
  * a4/a5 -- the device-resident prefix-cache table (Sec. 2.1; Table

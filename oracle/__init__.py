@@ -11,6 +11,8 @@ What it computes, each piece plainly and in the paper's order:
 * ``chain``        h_0 = H(tokens_0), h_j = H(h_{j-1}, tokens_j)   (Sec. 2.1)
                    root salting h_0 = H(sigma_p || tokens_0)       (Sec. 4.1)
                    boundary salting at block k                     (Sec. 4.2)
+* ``chain_from``   the same recurrence entered at block j0 from the parent
+                   digest h_{j0-1} (Sec. 2.1; Sec. 5.7, multi-turn sessions)
 * ``Table``        a set of block hashes; lookup returns the number of
                    leading blocks present, i.e. the first miss     (Sec. 2.1,
                    Table "tab:taxonomy", block prefix cache row)
@@ -20,8 +22,8 @@ package also carries its own FIPS 180-4 SHA-256 and RFC 2104 HMAC in plain
 Python (``fips_sha256``, ``rfc2104``), used by the tests to pin the library
 routines; all pins are listed in the tests.
 """
-from .kvgov import (NONE, ROOT, BOUNDARY, BLOCK, salts, block_bytes, chain,
-                    hash_chains, hash_chains_parallel, Table, lookup_hits)
+from .kvgov import (NONE, ROOT, BOUNDARY, BLOCK, salts, block_bytes, chain, chain_from,
+                    hash_chains, hash_chains_parallel, hash_chains_resume, Table, lookup_hits)
 
-__all__ = ["NONE", "ROOT", "BOUNDARY", "BLOCK", "salts", "block_bytes", "chain",
-           "hash_chains", "hash_chains_parallel", "Table", "lookup_hits"]
+__all__ = ["NONE", "ROOT", "BOUNDARY", "BLOCK", "salts", "block_bytes", "chain", "chain_from",
+           "hash_chains", "hash_chains_parallel", "hash_chains_resume", "Table", "lookup_hits"]

@@ -92,6 +92,58 @@ def chain(tokens: Sequence[int], mode: int, salt_bytes: Optional[bytes] = None,
     return out
 
 
+def chain_from(tokens: Sequence[int], start: int, parent: Optional[bytes], mode: int,
+               salt_bytes: Optional[bytes] = None, boundary_tok: Optional[int] = None,
+               hash_fn=sha256) -> List[bytes]:
+    """Block hashes h_start .. h_{n-1} of one request given h_{start-1}.
+
+    Sec. 2.1: each h_j is a function of h_{j-1}, T_j and (Sec. 4.1, 4.2) of
+    sigma_p on the salted block only, so the recurrence can be entered at any
+    block with its parent digest (Sec. 5.7: a later turn of a session
+    extends the earlier turn's prompt exactly).  ``parent`` is ignored when
+    start is 0; the salt of a block below ``start`` is already inside it."""
+    n_full = len(tokens) // BLOCK
+    if not 0 <= start <= n_full:
+        raise ValueError("start outside [0, len // 16]")
+    if start > 0 and (parent is None or len(parent) != DIGEST):
+        raise ValueError("resuming needs the 32-byte parent digest")
+    if mode == BOUNDARY:
+        if boundary_tok is None or not 0 <= boundary_tok <= len(tokens):
+            raise ValueError("boundary_tok outside [0, len]")
+        k = boundary_tok // BLOCK
+    elif mode in (NONE, ROOT):
+        k = 0 if mode == ROOT else None
+    else:
+        raise ValueError("unknown mode")
+    if mode != NONE and (salt_bytes is None or len(salt_bytes) != DIGEST):
+        raise ValueError("salted modes need a 32-byte salt")
+    out: List[bytes] = []
+    h = bytes(parent) if start > 0 else b""
+    for j in range(start, n_full):
+        sigma = salt_bytes if (k is not None and j == k) else b""
+        h = hash_fn(sigma + h + block_bytes(tokens, j))
+        out.append(h)
+    return out
+
+
+def hash_chains_resume(tokens, tok_offsets, principal, salt_list, mode, start, parents,
+                       boundary_tok=None) -> np.ndarray:
+    """``chain_from`` over a ragged batch, in the flat layout of the C ABI:
+    request r contributes rows for blocks start[r] .. len_r // 16 - 1."""
+    tok_offsets, n = _check_batch(tokens, tok_offsets, principal, len(salt_list), mode,
+                                  boundary_tok)
+    out = []
+    for r in range(n):
+        a, b = int(tok_offsets[r]), int(tok_offsets[r + 1])
+        s = salt_list[int(principal[r])] if mode != NONE else None
+        bt = int(boundary_tok[r]) if mode == BOUNDARY else None
+        par = bytes(np.asarray(parents[r], dtype=np.uint8).tobytes())
+        out.extend(chain_from(tokens[a:b], int(start[r]), par, mode, s, bt))
+    if not out:
+        return np.zeros((0, DIGEST), dtype=np.uint8)
+    return np.frombuffer(b"".join(out), dtype=np.uint8).reshape(-1, DIGEST)
+
+
 def _check_batch(tokens, tok_offsets, principal, P, mode, boundary_tok):
     tok_offsets = np.asarray(tok_offsets, dtype=np.int64)
     n = tok_offsets.shape[0] - 1

@@ -187,21 +187,24 @@ __global__ __launch_bounds__(64) void k_salts(SaltArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// output layout: blk_offsets = exclusive prefix sum of len // 16
+// output layout: blk_offsets = exclusive prefix sum of len // 16 (minus the
+// start block when resuming)
 // ---------------------------------------------------------------------------
 
 constexpr int kScanThreads = 256;
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kScanThreads * kScanItems;
 
-__device__ __forceinline__ int64_t req_blocks(const int64_t *tok_offsets, int64_t r,
-                                              int32_t *status) {
+// blocks hashed for request r: full blocks from start[r] on (start NULL: 0)
+__device__ __forceinline__ int64_t req_blocks(const int64_t *tok_offsets, const int32_t *start,
+                                              int64_t r, int32_t *status) {
   const int64_t len = tok_offsets[r + 1] - tok_offsets[r];
-  if (len < 0) {
+  const int64_t j0 = start ? start[r] : 0;
+  if (len < 0 || j0 < 0 || j0 > (len >> 4)) {
     latch(status, KVGOV_E_OFFSETS);
     return 0;
   }
-  return len >> 4;
+  return (len >> 4) - j0;
 }
 
 // inclusive scan across the 256 threads of a workgroup
@@ -221,7 +224,8 @@ __device__ __forceinline__ int64_t block_inclusive_scan(int64_t v, int64_t *lds_
 }
 
 __global__ __launch_bounds__(kScanThreads) void k_blk_partial(const int64_t *tok_offsets,
-                                                              int32_t n, int64_t *partial,
+                                                              const int32_t *start, int32_t n,
+                                                              int64_t *partial,
                                                               int32_t *status) {
   __shared__ int64_t lds[kScanThreads / 64];
   const int64_t base = (int64_t)blockIdx.x * kScanTile;
@@ -229,7 +233,7 @@ __global__ __launch_bounds__(kScanThreads) void k_blk_partial(const int64_t *tok
 #pragma unroll
   for (int i = 0; i < kScanItems; ++i) {
     const int64_t r = base + (int64_t)i * kScanThreads + threadIdx.x;
-    if (r < n) s += req_blocks(tok_offsets, r, status);
+    if (r < n) s += req_blocks(tok_offsets, start, r, status);
   }
   const int64_t inc = block_inclusive_scan(s, lds);
   if (threadIdx.x == kScanThreads - 1) partial[blockIdx.x] = inc;
@@ -253,7 +257,8 @@ __global__ __launch_bounds__(kScanThreads) void k_blk_scan_partials(int64_t *par
   }
 }
 
-__global__ __launch_bounds__(kScanThreads) void k_blk_write(const int64_t *tok_offsets, int32_t n,
+__global__ __launch_bounds__(kScanThreads) void k_blk_write(const int64_t *tok_offsets,
+                                                            const int32_t *start, int32_t n,
                                                             const int64_t *partial,
                                                             int64_t *blk_offsets,
                                                             int32_t *status) {
@@ -266,7 +271,7 @@ __global__ __launch_bounds__(kScanThreads) void k_blk_write(const int64_t *tok_o
 #pragma unroll
   for (int i = 0; i < kScanItems; ++i) {
     const int64_t r = r0 + i;
-    c[i] = r < n ? req_blocks(tok_offsets, r, status) : 0;
+    c[i] = r < n ? req_blocks(tok_offsets, start, r, status) : 0;
     s += c[i];
   }
   const int64_t inc = block_inclusive_scan(s, lds);
@@ -287,9 +292,11 @@ __global__ __launch_bounds__(kScanThreads) void k_blk_write(const int64_t *tok_o
 
 constexpr int kOrderBuckets = 4096;  // block counts >= 4095 share the top bucket
 
-__device__ __forceinline__ int order_bucket(const int64_t *tok_offsets, int32_t r) {
-  const int64_t len = tok_offsets[r + 1] - tok_offsets[r];
-  const int64_t nb = len > 0 ? (len >> 4) : 0;
+// bucket of request r: the blocks it hashes, from the block offsets (any
+// values are safe here; the chain kernels validate them)
+__device__ __forceinline__ int order_bucket(const int64_t *blk_offsets, int32_t r) {
+  const int64_t d = blk_offsets[r + 1] - blk_offsets[r];
+  const int64_t nb = d > 0 ? d : 0;
   return (int)(nb < kOrderBuckets - 1 ? nb : kOrderBuckets - 1);
 }
 
@@ -301,7 +308,7 @@ constexpr int kOrderThreads = 1024;
 constexpr int kOrderPerThread = 4;
 constexpr int64_t kOrderTile = (int64_t)kOrderThreads * kOrderPerThread;
 
-__global__ __launch_bounds__(kOrderThreads) void k_order_hist(const int64_t *tok_offsets,
+__global__ __launch_bounds__(kOrderThreads) void k_order_hist(const int64_t *blk_offsets,
                                                               int32_t n, int32_t *hist) {
   __shared__ int32_t h[kOrderBuckets];
   for (int i = threadIdx.x; i < kOrderBuckets; i += kOrderThreads) h[i] = 0;
@@ -310,7 +317,7 @@ __global__ __launch_bounds__(kOrderThreads) void k_order_hist(const int64_t *tok
 #pragma unroll
   for (int k = 0; k < kOrderPerThread; ++k) {
     const int64_t r = base + (int64_t)k * kOrderThreads + threadIdx.x;
-    if (r < n) atomicAdd(&h[order_bucket(tok_offsets, (int32_t)r)], 1);
+    if (r < n) atomicAdd(&h[order_bucket(blk_offsets, (int32_t)r)], 1);
   }
   __syncthreads();
   for (int i = threadIdx.x; i < kOrderBuckets; i += kOrderThreads)
@@ -339,7 +346,7 @@ __global__ __launch_bounds__(256) void k_order_scan(int32_t *hist) {
   }
 }
 
-__global__ __launch_bounds__(kOrderThreads) void k_order_scatter(const int64_t *tok_offsets,
+__global__ __launch_bounds__(kOrderThreads) void k_order_scatter(const int64_t *blk_offsets,
                                                                  int32_t n, int32_t *cursor,
                                                                  int32_t *order) {
   __shared__ int32_t cnt[kOrderBuckets];
@@ -353,7 +360,7 @@ __global__ __launch_bounds__(kOrderThreads) void k_order_scatter(const int64_t *
     const int64_t r = base + (int64_t)k * kOrderThreads + threadIdx.x;
     bucket[k] = -1;
     if (r < n) {
-      bucket[k] = order_bucket(tok_offsets, (int32_t)r);
+      bucket[k] = order_bucket(blk_offsets, (int32_t)r);
       rank[k] = atomicAdd(&cnt[bucket[k]], 1);
     }
   }
@@ -393,17 +400,24 @@ struct ChainArgs {
   int64_t n_blocks;
   const int32_t *order;  // NULL: request i on lane i
   int32_t *status;
+  // chain extension: request r resumes at block start[r] from the parent
+  // digest parents[r] (NULL: every chain starts at block 0)
+  const int32_t *start;
+  const uint8_t *parents;
 };
 
 // Per-request set-up shared by both chain kernels.  Returns false (after
 // latching the error) for a request that must write nothing.
 struct ChainReq {
-  const int32_t *tp;  // first token
-  uint8_t *out;       // first output row
-  int64_t nf;         // full blocks
+  const int32_t *tp;  // tokens of the first block hashed
+  uint8_t *out;       // its output row
+  int64_t nf;         // blocks to hash (full blocks from the start block on)
+  int64_t j0;         // the start block (0 unless resuming)
   int64_t k;          // salted block (boundary mode), else -1
+  int64_t kr;         // iteration (block kr + j0) of a boundary block still to
+                      // hash with sigma || h, else -1
   uint32_t sig[8];    // salt as state words (salted modes)
-  bool salted_root;   // first block carries the salt (root, or boundary k = 0)
+  bool salted_root;   // block 0 carries the salt (root, or boundary k = 0)
 };
 
 template <int MODE>
@@ -414,7 +428,13 @@ __device__ __forceinline__ bool chain_setup(const ChainArgs &a, int32_t r, Chain
     return false;
   }
   const int64_t len = t1 - t0;
-  q.nf = len >> 4;
+  const int64_t full = len >> 4;
+  q.j0 = a.start ? a.start[r] : 0;
+  if (q.j0 < 0 || q.j0 > full) {
+    latch(a.status, KVGOV_E_OFFSETS);
+    return false;
+  }
+  q.nf = full - q.j0;
   const int64_t b0 = a.blk_offsets[r];
   if (b0 < 0 || a.blk_offsets[r + 1] - b0 != q.nf || b0 + q.nf > a.n_blocks) {
     latch(a.status, KVGOV_E_OFFSETS);
@@ -439,9 +459,10 @@ __device__ __forceinline__ bool chain_setup(const ChainArgs &a, int32_t r, Chain
     }
     q.k = bt >> 4;
   }
-  q.tp = a.tokens + t0;
+  q.tp = a.tokens + t0 + 16 * q.j0;
   q.out = a.hashes + b0 * 32;
   q.salted_root = (MODE == KVGOV_ROOT) || (MODE == KVGOV_BOUNDARY && q.k == 0);
+  q.kr = q.k > 0 && q.k >= q.j0 ? q.k - q.j0 : -1;
   return true;
 }
 
@@ -496,21 +517,27 @@ __device__ __forceinline__ void single_chain(const ChainArgs &a, int32_t i) {
   if (!chain_setup<MODE>(a, r, q) || q.nf == 0) return;
   const int64_t nf = q.nf;
 
-  // H holds h_{j-1} as state words; a root-salted first block (and k == 0 in
-  // boundary mode) is the usual pattern with sigma in place of h_{-1}.
+  // H holds h_{j-1} as state words: the parent digest when resuming; a
+  // root-salted first block (and k == 0 in boundary mode) is the usual
+  // pattern with sigma in place of h_{-1}.
   uint32_t H[8];
+  if (q.j0 > 0) {
+    load_digest(a.parents + (int64_t)r * 32, H);
+  } else {
 #pragma unroll
-  for (int w = 0; w < 8; ++w) H[w] = q.salted_root ? q.sig[w] : 0u;
+    for (int w = 0; w < 8; ++w) H[w] = q.salted_root ? q.sig[w] : 0u;
+  }
 
   u32x4 nxt[4];
   uint32_t T[16];  // tokens of block j
   load_raw(q.tp, nxt);
   take_block(nxt, T, q.tp, 0, nf);
-  const bool plain_first = !q.salted_root;
+  const bool plain_first = !q.salted_root && q.j0 == 0;
 
+  // iteration j hashes block q.j0 + j of the chain
   for (int64_t j = 0; j < nf; ++j) {
     const bool u0 = plain_first && j == 0;
-    const bool bnd = (MODE == KVGOV_BOUNDARY) && j == q.k && q.k > 0;
+    const bool bnd = (MODE == KVGOV_BOUNDARY) && j == q.kr;
     if (MODE == KVGOV_ROOT || !__any(u0 || bnd)) {
       // hot path: (IV; h || T[0..7]) then (state; T[8..15] || pad96)
       uint32_t st[8], w[16];
@@ -547,7 +574,7 @@ __global__ __launch_bounds__(256) void k_chains(ChainArgs a) {
 // iterations over all requests of the workgroup.
 struct ReqPeek {
   int64_t nf;
-  int64_t k;
+  int64_t kr;  // iteration of the boundary block, else -1
 };
 
 template <int MODE>
@@ -556,7 +583,7 @@ __device__ __forceinline__ ReqPeek req_peek(const ChainArgs &a, int32_t i) {
   if (i < a.n) {
     ChainReq q;
     const int32_t r = a.order ? a.order[i] : i;
-    if (chain_setup<MODE>(a, r, q)) p = ReqPeek{q.nf, q.k};
+    if (chain_setup<MODE>(a, r, q)) p = ReqPeek{q.nf, q.kr};
   }
   return p;
 }
@@ -873,7 +900,7 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
     ok = chain_setup<MODE>(a, r, q);
   }
   const int64_t nf = ok ? q.nf : 0;
-  const int64_t kb = ok ? q.k : -1;  // boundary block (boundary mode), else -1
+  const int64_t kb = ok ? q.kr : -1;  // boundary iteration (boundary mode), else -1
   // Trip count and boundary iterations are decided over all 64 requests of
   // the workgroup: the schedule wave holds them all, and a rounds lane also
   // looks at the request of the same lane in the other rounds wave.
@@ -920,12 +947,17 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
     uint32_t T0[16];
     take_block(nxt, T0, tp, 0, nfl);
     if (nf > 0) {
-      const bool salted = q.salted_root;
-      if (salted) {
+      // h_{j0-1}: the parent digest when resuming (in the second half of a
+      // boundary block's first message), sigma for a salted root
+      const bool resume = q.j0 > 0, bnd0 = MODE == KVGOV_BOUNDARY && kb == 0;
+      if (resume || q.salted_root) {
+        uint32_t h[8];
+        if (resume)
+          load_digest(a.parents + (int64_t)(a.order ? a.order[i] : i) * 32, h);
 #pragma unroll
-        for (int x = 0; x < 8; ++x) L.ha[x][lane] = q.sig[x];  // h_{-1} = sigma
+        for (int x = 0; x < 8; ++x) (bnd0 ? L.hb : L.ha)[x][lane] = resume ? h[x] : q.sig[x];
       }
-      lp_prepare(T0, q.sig, !salted, false, L, 0, lane);
+      lp_prepare(T0, q.sig, !resume && !q.salted_root, bnd0, L, 0, lane);
     }
   }
   __syncthreads();
@@ -937,8 +969,7 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
     // boundary blocks take a third compression (workgroup-uniform decision)
     bool third = false;
     if (MODE == KVGOV_BOUNDARY) {
-      const bool mine_bnd = (j < own.nf && j == own.k && own.k > 0) ||
-                            (j < other.nf && j == other.k && other.k > 0);
+      const bool mine_bnd = (j < own.nf && j == own.kr) || (j < other.nf && j == other.kr);
       third = __any(mine_bnd);
     }
 
@@ -998,13 +1029,13 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
           for (int x = 0; x < 4; ++x) st3[x] = st[x];
           lp_load16(k3, L.c3, 0, col3);
           lp_compress_rows(st3, k3, L.c3, col3, c, a_lane);
-          const bool bnd = j == kb && kb > 0;
+          const bool bnd = j == kb;
 #pragma unroll
           for (int x = 0; x < 4; ++x) st[x] = bnd ? st3[x] : st[x];
         }
         // h_j: the next block's first message words 0..7 (plain), or 8..15
         // (the next block is the boundary block)
-        const bool next_bnd = MODE == KVGOV_BOUNDARY && kb > 0 && j + 1 == kb;
+        const bool next_bnd = MODE == KVGOV_BOUNDARY && j + 1 == kb;
         uint32_t(*hrows)[kLpCols] = next_bnd ? L.hb : L.ha;
 #pragma unroll
         for (int x = 0; x < 4; ++x) hrows[half + x][mine] = st[x];
@@ -1034,7 +1065,7 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
         const int64_t jn = j + 1 < nfl ? j + 1 : nfl - 1;
         take_block(nxt, Tn, tp, jn, nfl);
         if (next) {
-          const bool bnd_next = MODE == KVGOV_BOUNDARY && kb > 0 && j + 1 == kb;
+          const bool bnd_next = MODE == KVGOV_BOUNDARY && j + 1 == kb;
           lp_prepare(Tn, q.sig, false, bnd_next, L, nb, lane);
         }
       }
@@ -1186,8 +1217,9 @@ int kvgov_salts(const uint8_t *K, size_t K_len, const uint8_t *principal_ids, in
   return rc;
 }
 
-int kvgov_block_offsets(const int64_t *tok_offsets, int32_t n, int32_t block_size,
-                        int64_t *blk_offsets, int32_t *status, void *stream) {
+static int block_offsets_impl(const int64_t *tok_offsets, const int32_t *start, int32_t n,
+                              int32_t block_size, int64_t *blk_offsets, int32_t *status,
+                              void *stream) {
   if (!tok_offsets || !blk_offsets || !status || n < 0) return KVGOV_E_INVAL;
   if (block_size != KVGOV_BLOCK_SIZE) return KVGOV_E_UNSUPPORTED;
   hipStream_t s = as_stream(stream);
@@ -1197,13 +1229,25 @@ int kvgov_block_offsets(const int64_t *tok_offsets, int32_t n, int32_t block_siz
       hipSuccess)
     return KVGOV_E_NOMEM;
   hipLaunchKernelGGL(k_blk_partial, dim3((unsigned)tiles), dim3(kScanThreads), 0, s,
-                     tok_offsets, n, partial, status);
+                     tok_offsets, start, n, partial, status);
   hipLaunchKernelGGL(k_blk_scan_partials, dim3(1), dim3(kScanThreads), 0, s, partial, tiles);
   hipLaunchKernelGGL(k_blk_write, dim3((unsigned)tiles), dim3(kScanThreads), 0, s, tok_offsets,
-                     n, partial, blk_offsets, status);
+                     start, n, partial, blk_offsets, status);
   int rc = launch_status();
   if (hipFreeAsync(partial, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
   return rc;
+}
+
+int kvgov_block_offsets(const int64_t *tok_offsets, int32_t n, int32_t block_size,
+                        int64_t *blk_offsets, int32_t *status, void *stream) {
+  return block_offsets_impl(tok_offsets, nullptr, n, block_size, blk_offsets, status, stream);
+}
+
+int kvgov_resume_offsets(const int64_t *tok_offsets, const int32_t *start_block, int32_t n,
+                         int32_t block_size, int64_t *blk_offsets, int32_t *status,
+                         void *stream) {
+  if (n > 0 && !start_block) return KVGOV_E_INVAL;
+  return block_offsets_impl(tok_offsets, start_block, n, block_size, blk_offsets, status, stream);
 }
 
 // Longest-first ordering pays once the batch has about as many waves as the
@@ -1213,11 +1257,12 @@ int kvgov_block_offsets(const int64_t *tok_offsets, int32_t n, int32_t block_siz
 // ordered.)
 static int64_t order_min_requests() { return (int64_t)device_cu_count() * 4 * kWave / 2; }
 
-int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_offsets,
-                      int32_t n, const int32_t *principal, const uint8_t *salts, int32_t P,
-                      int32_t mode, const int32_t *boundary_tok, int32_t block_size,
-                      const int64_t *blk_offsets, uint8_t *hashes, int64_t n_blocks,
-                      int32_t *status, void *stream) {
+static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_offsets,
+                            int32_t n, const int32_t *principal, const uint8_t *salts, int32_t P,
+                            int32_t mode, const int32_t *boundary_tok, int32_t block_size,
+                            const int32_t *start, const uint8_t *parents,
+                            const int64_t *blk_offsets, uint8_t *hashes, int64_t n_blocks,
+                            int32_t *status, void *stream) {
   if (n < 0 || n_tokens < 0 || n_blocks < 0 || !status) return KVGOV_E_INVAL;
   if (mode != KVGOV_NONE && mode != KVGOV_ROOT && mode != KVGOV_BOUNDARY) return KVGOV_E_INVAL;
   if (block_size != KVGOV_BLOCK_SIZE) return KVGOV_E_UNSUPPORTED;
@@ -1244,6 +1289,8 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
   a.n_blocks = n_blocks;
   a.status = status;
   a.order = nullptr;
+  a.start = start;
+  a.parents = parents;
 
   const int slots = lp_slots(n);
   int32_t *scratch = nullptr;
@@ -1256,9 +1303,9 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
     hipLaunchKernelGGL(k_fill_i32, dim3(kOrderBuckets / 256), dim3(256), 0, s, hist,
                        (int64_t)kOrderBuckets, 0);
     const dim3 tiles((unsigned)ceil_div(n, kOrderTile));
-    hipLaunchKernelGGL(k_order_hist, tiles, dim3(kOrderThreads), 0, s, tok_offsets, n, hist);
+    hipLaunchKernelGGL(k_order_hist, tiles, dim3(kOrderThreads), 0, s, blk_offsets, n, hist);
     hipLaunchKernelGGL(k_order_scan, dim3(1), dim3(256), 0, s, hist);
-    hipLaunchKernelGGL(k_order_scatter, tiles, dim3(kOrderThreads), 0, s, tok_offsets, n, hist,
+    hipLaunchKernelGGL(k_order_scatter, tiles, dim3(kOrderThreads), 0, s, blk_offsets, n, hist,
                        order);
     a.order = order;
   }
@@ -1305,6 +1352,29 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
   int rc = launch_status();
   if (scratch && hipFreeAsync(scratch, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
   return rc;
+}
+
+int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_offsets,
+                      int32_t n, const int32_t *principal, const uint8_t *salts, int32_t P,
+                      int32_t mode, const int32_t *boundary_tok, int32_t block_size,
+                      const int64_t *blk_offsets, uint8_t *hashes, int64_t n_blocks,
+                      int32_t *status, void *stream) {
+  return hash_chains_impl(tokens, n_tokens, tok_offsets, n, principal, salts, P, mode,
+                          boundary_tok, block_size, nullptr, nullptr, blk_offsets, hashes,
+                          n_blocks, status, stream);
+}
+
+int kvgov_hash_chains_resume(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_offsets,
+                             int32_t n, const int32_t *principal, const uint8_t *salts,
+                             int32_t P, int32_t mode, const int32_t *boundary_tok,
+                             int32_t block_size, const int32_t *start_block,
+                             const uint8_t *parents, const int64_t *blk_offsets, uint8_t *hashes,
+                             int64_t n_blocks, int32_t *status, void *stream) {
+  if (n > 0 && (!start_block || !parents)) return KVGOV_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(parents) & 3) return KVGOV_E_INVAL;
+  return hash_chains_impl(tokens, n_tokens, tok_offsets, n, principal, salts, P, mode,
+                          boundary_tok, block_size, start_block, parents, blk_offsets, hashes,
+                          n_blocks, status, stream);
 }
 
 }  // extern "C"

@@ -11,6 +11,8 @@ Calls mirror the C ABI one to one:
     kvgov_salts         -> salts(K, principal_ids)
     kvgov_block_offsets -> block_offsets(tok_offsets)
     kvgov_hash_chains   -> hash_chains(tokens, tok_offsets, principal, salts, mode, ...)
+    kvgov_hash_chains_resume -> hash_chains_resume(..., start_block, parents, ...)
+    kvgov_resume_offsets -> resume_offsets(tok_offsets, start_block)
     kvgov_cache_*       -> Cache(log2_slots).insert / lookup / clear / count / export
 """
 from __future__ import annotations
@@ -39,6 +41,10 @@ _SIGNATURES = {
     "kvgov_block_offsets": (ctypes.c_int, [_vp, _c_i32, _c_i32, _vp, _vp, _vp]),
     "kvgov_hash_chains": (ctypes.c_int, [_vp, _c_i64, _vp, _c_i32, _vp, _vp, _c_i32, _c_i32,
                                          _vp, _c_i32, _vp, _vp, _c_i64, _vp, _vp]),
+    "kvgov_hash_chains_resume": (ctypes.c_int, [_vp, _c_i64, _vp, _c_i32, _vp, _vp, _c_i32,
+                                                _c_i32, _vp, _c_i32, _vp, _vp, _vp, _vp,
+                                                _c_i64, _vp, _vp]),
+    "kvgov_resume_offsets": (ctypes.c_int, [_vp, _vp, _c_i32, _c_i32, _vp, _vp, _vp]),
     "kvgov_cache_create": (ctypes.c_int, [_c_i32, ctypes.POINTER(_vp)]),
     "kvgov_cache_destroy": (ctypes.c_int, [_vp]),
     "kvgov_cache_clear": (ctypes.c_int, [_vp, _vp]),
@@ -203,6 +209,64 @@ def hash_chains(tokens: torch.Tensor, tok_offsets: torch.Tensor, principal: Opti
                                    _stream(stream)), "kvgov_hash_chains")
     if check:
         check_status(status, "kvgov_hash_chains")
+    return out
+
+
+def resume_offsets(tok_offsets: torch.Tensor, start_block: torch.Tensor,
+                   out: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None,
+                   stream=None) -> torch.Tensor:
+    to = _dev(tok_offsets, torch.int64, "tok_offsets")
+    sb = _dev(start_block, torch.int32, "start_block")
+    n = to.numel() - 1
+    if sb.numel() != n:
+        raise ValueError("start_block must hold one entry per request")
+    if out is None:
+        out = torch.empty(n + 1, dtype=torch.int64, device=to.device)
+    own = status is None
+    if own:
+        status = new_status(to.device)
+    _check(lib().kvgov_resume_offsets(_ptr(to), _ptr(sb), n, BLOCK, _ptr(out), _ptr(status),
+                                      _stream(stream)), "kvgov_resume_offsets")
+    if own:
+        check_status(status, "kvgov_resume_offsets")
+    return out
+
+
+def hash_chains_resume(tokens: torch.Tensor, tok_offsets: torch.Tensor,
+                       principal: Optional[torch.Tensor], salt_table: Optional[torch.Tensor],
+                       mode: int, start_block: torch.Tensor, parents: torch.Tensor,
+                       boundary_tok: Optional[torch.Tensor] = None,
+                       blk_offsets: Optional[torch.Tensor] = None,
+                       out: Optional[torch.Tensor] = None, status: Optional[torch.Tensor] = None,
+                       check: bool = True, stream=None) -> torch.Tensor:
+    """Blocks start_block[r] .. len_r // 16 - 1 of each chain, resumed from
+    parents[r] = h_{start_block[r] - 1}; uint8 [blk_offsets[-1], 32]."""
+    tk = _dev(tokens, torch.int32, "tokens")
+    to = _dev(tok_offsets, torch.int64, "tok_offsets")
+    n = to.numel() - 1
+    pr = _dev(principal, torch.int32, "principal", allow_none=(mode == NONE))
+    st = _dev(salt_table, torch.uint8, "salts", allow_none=(mode == NONE))
+    bt = _dev(boundary_tok, torch.int32, "boundary_tok", allow_none=(mode != BOUNDARY))
+    sb = _dev(start_block, torch.int32, "start_block")
+    pa = _dev(parents, torch.uint8, "parents")
+    if sb.numel() != n or pa.numel() != 32 * n:
+        raise ValueError("start_block and parents must hold one entry per request")
+    P = 0 if st is None else int(st.shape[0])
+    if status is None:
+        status = new_status(tk.device)
+    if blk_offsets is None:
+        blk_offsets = resume_offsets(to, sb, status=status, stream=stream)
+    bo = _dev(blk_offsets, torch.int64, "blk_offsets")
+    if out is None:
+        out = torch.empty((int(bo[-1].item()), 32), dtype=torch.uint8, device=tk.device)
+    _dev(out, torch.uint8, "out")
+    _check(lib().kvgov_hash_chains_resume(_ptr(tk), tk.numel(), _ptr(to), n, _ptr(pr), _ptr(st),
+                                          P, int(mode), _ptr(bt), BLOCK, _ptr(sb), _ptr(pa),
+                                          _ptr(bo), _ptr(out), out.shape[0] if out.dim() else 0,
+                                          _ptr(status), _stream(stream)),
+           "kvgov_hash_chains_resume")
+    if check:
+        check_status(status, "kvgov_hash_chains_resume")
     return out
 
 

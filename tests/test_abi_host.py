@@ -87,6 +87,28 @@ def test_host_validation_returns_before_any_launch():
     assert chains(tokens=ctypes.c_void_p(0x1002)) == INVAL  # misaligned
     assert chains(hashes=ctypes.c_void_p(0x1001)) == INVAL
     assert chains(n=0) == 0
+
+    def resume(**kw):
+        a = dict(tokens=fake, n_tokens=64, tok_offsets=fake, n=2, principal=fake, salts=fake,
+                 P=4, mode=K.ROOT, boundary_tok=fake, block_size=16, start_block=fake,
+                 parents=fake, blk_offsets=fake, hashes=fake, n_blocks=4, status=fake,
+                 stream=None)
+        a.update(kw)
+        return L.kvgov_hash_chains_resume(*a.values())
+
+    assert resume(start_block=None) == INVAL
+    assert resume(parents=None) == INVAL
+    assert resume(parents=ctypes.c_void_p(0x1002)) == INVAL  # misaligned
+    assert resume(n=-1) == INVAL
+    assert resume(mode=3) == INVAL
+    assert resume(block_size=8) == UNSUP
+    assert resume(status=None) == INVAL
+    assert resume(P=0) == INVAL
+    assert resume(n=0, start_block=None, parents=None) == 0
+    assert L.kvgov_resume_offsets(fake, None, 4, 16, fake, fake, None) == INVAL
+    assert L.kvgov_resume_offsets(None, fake, 4, 16, fake, fake, None) == INVAL
+    assert L.kvgov_resume_offsets(fake, fake, 4, 8, fake, fake, None) == UNSUP
+    assert L.kvgov_resume_offsets(fake, fake, -1, 16, fake, fake, None) == INVAL
     # cache
     h = ctypes.c_void_p()
     assert L.kvgov_cache_create(3, ctypes.byref(h)) == INVAL
