@@ -27,8 +27,10 @@ longest request hashed alone), the device's measured peaks (integer-VALU and
 those, and the CPU oracle per phase, on one core and with the host's CPU
 model and SHA extension flag.
 
---config {tiny,template,large} runs the same kind of step on those
-workloads (large: chains + insert + a re-lookup of the inserted batch);
+--config {tiny,template,large,session} runs the same kind of step on those
+workloads (large: chains + insert + a re-lookup of the inserted batch;
+session: turn-2 chains resumed at turn 1's last full block from its digest,
+insert and re-lookup of the new blocks, and the full rehash timed beside);
 --config probe times lookups alone against the 8M-key resident table (the
 resident chains, the probe chains and the insert are done before timing).
 Only the default is the bench line; the others are for the per-config table.
@@ -86,6 +88,9 @@ DESCRIPTIONS = {
              "1M probes of U{{8..64}} blocks, 70% own-principal prefixes, 30% foreign",
     "large": "large batch: 65536 requests, lognormal lengths (median 2048, sigma 1, max "
              "32768 tokens), 4096 principals, root and boundary; chains + insert + re-lookup",
+    "session": "multi-turn sessions: 4096 turn-2 prompts (paper-shaped turn 1 + U{{64..1024}} "
+               "follow-up tokens), 64 principals, root and boundary (token 2119); chains "
+               "resumed at turn 1's last full block + insert + re-lookup of the new blocks",
 }
 
 
@@ -129,21 +134,34 @@ def recorded_traffic(kernel: str, workload: str, group: str):
     return None
 
 
-def compressions(batch: W.Batch, mode: int) -> int:
-    """Compressions the definition needs: 2 per full block, plus one for the
-    128-byte boundary block (boundary mode, 0 < k < n_full)."""
+def start_blocks(wl: W.Workload, batch: W.Batch) -> np.ndarray:
+    """Block each request's hashing starts at: turn 1's full-block count for
+    the resumed sessions, else 0."""
+    st = wl.notes.get("start") if wl.name == "session" else None
+    return np.zeros(batch.n, np.int64) if st is None else np.asarray(st, np.int64)
+
+
+def hashed_counts(wl: W.Workload, batch: W.Batch) -> np.ndarray:
+    """Blocks hashed (and inserted / looked up) per request."""
+    return batch.block_counts() - start_blocks(wl, batch)
+
+
+def compressions(wl: W.Workload, batch: W.Batch, mode: int) -> int:
+    """Compressions the definition needs: 2 per hashed block, plus one for
+    the 128-byte boundary block (boundary mode, 0 < k < n_full, k at or
+    after the start block)."""
     nf = batch.block_counts()
-    c = 2 * int(nf.sum())
+    j0 = start_blocks(wl, batch)
+    c = 2 * int((nf - j0).sum())
     if mode == W.BOUNDARY:
         k = batch.boundary_tok.astype(np.int64) // W.BLOCK
-        c += int(((k > 0) & (k < nf)).sum())
+        c += int(((k > 0) & (k < nf) & (k >= j0)).sum())
     return c
 
 
-def lookup_bytes(batch: W.Batch, hits: np.ndarray) -> int:
-    nf = batch.block_counts()
-    examined = np.minimum(hits.astype(np.int64) + 1, nf)
-    return int(examined.sum()) * LOOKUP_BYTES_PER_BLOCK + batch.n * LOOKUP_BYTES_PER_REQUEST
+def lookup_bytes(counts: np.ndarray, hits: np.ndarray) -> int:
+    examined = np.minimum(hits.astype(np.int64) + 1, counts)
+    return int(examined.sum()) * LOOKUP_BYTES_PER_BLOCK + counts.size * LOOKUP_BYTES_PER_REQUEST
 
 
 def concat(A: W.Batch, B: W.Batch) -> W.Batch:
@@ -194,6 +212,8 @@ def cpu_baseline(wl: W.Workload, processes: int, max_blocks: int):
     import oracle as O
     if wl.name == "probe":
         return cpu_baseline_probe(wl, processes)
+    if wl.name == "session":
+        return cpu_baseline_session(wl, processes)
     same = wl.name == "large"
     A = capped(wl.insert, max_blocks)
     B = A if same else capped(wl.lookup, max_blocks)
@@ -249,6 +269,55 @@ def cpu_baseline(wl: W.Workload, processes: int, max_blocks: int):
                 "sample": f"chains of the first {one.n} insert requests, "
                           f"{W.MODE_NAMES[wl.modes[0]]} mode",
                 "salts_us_per_key": cpu_salt_cost(wl) * 1e6,
+            },
+            "host": host_cpu_info()}
+
+
+def cpu_baseline_session(wl: W.Workload, processes: int):
+    """The oracle's resumed chains (chain_from, one process) of every turn-2
+    prompt, then the insert and re-lookup of the new blocks; turn 1's chains,
+    which give the parents, are hashed before timing."""
+    import oracle as O
+    A = wl.insert
+    T1 = wl.notes["turn1"]
+    start = wl.notes["start"]
+    clock = time.perf_counter
+    t = {"salts": 0.0, "chains": 0.0, "insert": 0.0, "lookup": 0.0}
+    t0 = clock()
+    salts = O.salts(wl.K, wl.principal_ids)
+    t["salts"] = clock() - t0
+    cnt = hashed_counts(wl, A)
+    bo = np.concatenate([[0], np.cumsum(cnt)]).astype(np.int64)
+    last = np.maximum(T1.blk_offsets()[1:] - 1, 0)
+    tokens = lookups = 0
+    for mode in wl.modes:
+        h1 = O.hash_chains_parallel(T1.tokens, T1.tok_offsets, T1.principal, salts, mode,
+                                    T1.boundary_tok, processes=processes)
+        parents = h1[last]
+        t0 = clock()
+        h = O.hash_chains_resume(A.tokens, A.tok_offsets, A.principal, salts, mode, start,
+                                 parents, A.boundary_tok)
+        t["chains"] += clock() - t0
+        tokens += 16 * int(cnt.sum())
+        T = O.Table()
+        t0 = clock()
+        T.insert(h, bo)
+        t["insert"] += clock() - t0
+        t0 = clock()
+        T.lookup(h, bo)
+        t["lookup"] += clock() - t0
+        lookups += A.n
+    dt = sum(t.values())
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": (f"one full step of the same workload ({tokens} block tokens hashed "
+                       f"from the start blocks, {lookups} lookups, {len(wl.modes)} modes) in "
+                       f"{dt:.1f} s, one process; turn 1's chains (the parents) not timed"),
+            "seconds": dt, "lookups_per_s": lookups / dt,
+            "phases": {
+                "salts_us_per_key": t["salts"] / wl.P * 1e6,
+                "chains_tokens_per_s": tokens / t["chains"],
+                "insert_keys_per_s": tokens / 16 / t["insert"],
+                "lookup_lookups_per_s": lookups / t["lookup"],
             },
             "host": host_cpu_info()}
 
@@ -367,14 +436,20 @@ def main():
     ids = to(wl.principal_ids)
     A = wl.insert
     probe_only = wl.name == "probe"
-    relookup_same = wl.name == "large"  # the lookup re-probes the inserted batch
+    session = wl.name == "session"  # chains resumed from turn 1's digests
+    # the lookup re-probes the inserted batch
+    relookup_same = wl.name in ("large", "session")
     B = A if relookup_same else wl.lookup
     X = A if relookup_same else concat(A, B)  # what one hashing call covers
-    nA = int(A.block_counts().sum())
-    nX = int(X.block_counts().sum())
+    cntX, cntB = hashed_counts(wl, X), hashed_counts(wl, B)
+    nA = int(hashed_counts(wl, A).sum())
+    nX = int(cntX.sum())
+    boX = np.concatenate([[0], np.cumsum(cntX)]).astype(np.int64)
     x = dict(tokens=to(X.tokens), tok_offsets=to(X.tok_offsets), principal=to(X.principal),
-             boundary_tok=to(X.boundary_tok), blk_offsets=to(X.blk_offsets()))
-    boA, boB = to(A.blk_offsets()), to(B.blk_offsets())
+             boundary_tok=to(X.boundary_tok), blk_offsets=to(boX))
+    boA = boB = x["blk_offsets"]
+    if not relookup_same:
+        boA, boB = to(A.blk_offsets()), to(B.blk_offsets())
     modes = wl.modes
     out = {m: torch.empty((nX, 32), dtype=torch.uint8, device=dev) for m in modes}
     hits = {m: torch.empty(B.n, dtype=torch.int32, device=dev) for m in modes}
@@ -387,6 +462,35 @@ def main():
 
     def bview(m):
         return out[m][0:nA], (out[m][0:nA] if relookup_same else out[m][nA:])
+
+    parents = {}
+    if session:
+        # untimed set-up: turn 1 hashed whole; each session's parent is the
+        # digest of turn 1's last full block (rows of empty turns are unused)
+        T1 = wl.notes["turn1"]
+        x["start"] = to(wl.notes["start"])
+        K.salts(wl.K, ids, out=salts)
+        last = to(np.maximum(T1.blk_offsets()[1:] - 1, 0))
+        for m in modes:
+            h1 = K.hash_chains(to(T1.tokens), to(T1.tok_offsets), to(T1.principal), salts, m,
+                               to(T1.boundary_tok))
+            parents[m] = h1[last].contiguous()
+            del h1
+        torch.cuda.synchronize()
+
+    def hash_call(m, s, xx=None, out_=None, par=None):
+        xx = x if xx is None else xx
+        if session:
+            K.hash_chains_resume(xx["tokens"], xx["tok_offsets"], xx["principal"], salts, m,
+                                 xx["start"], parents[m] if par is None else par,
+                                 xx["boundary_tok"], blk_offsets=xx["blk_offsets"],
+                                 out=out[m] if out_ is None else out_, status=status,
+                                 check=False, stream=s)
+        else:
+            K.hash_chains(xx["tokens"], xx["tok_offsets"], xx["principal"], salts, m,
+                          xx["boundary_tok"], blk_offsets=xx["blk_offsets"],
+                          out=out[m] if out_ is None else out_, status=status, check=False,
+                          stream=s)
 
     probe_hash_ms = None
     if probe_only:
@@ -439,9 +543,7 @@ def main():
                     e0 = torch.cuda.Event(enable_timing=True)
                     e1 = torch.cuda.Event(enable_timing=True)
                     e0.record(s)
-                K.hash_chains(x["tokens"], x["tok_offsets"], x["principal"], salts, m,
-                              x["boundary_tok"], blk_offsets=x["blk_offsets"], out=out[m],
-                              status=status, check=False, stream=s)
+                hash_call(m, s)
                 if record:
                     e1.record(s)
                     ev_chain.append((m, e0, e1))
@@ -480,7 +582,9 @@ def main():
     n_keys = {W.MODE_NAMES[m]: caches[m].count() for m in modes}
     gates = {}
     got_hits = {m: hits[m].cpu().numpy() for m in modes}
-    exp = B.expect_hits
+    # a re-lookup of the inserted batch takes its expected hits from the
+    # lookup batch the workload built for it
+    exp = (wl.lookup if relookup_same else B).expect_hits
     if exp is not None:
         gates["G4_hits_by_construction"] = all(
             bool(np.array_equal(got_hits[m], exp[m])) for m in modes)
@@ -488,13 +592,16 @@ def main():
     osalts = O.salts(wl.K, wl.principal_ids)
     gs = np.random.default_rng(7)
     ok = bytes(salts.cpu().numpy().tobytes()) == b"".join(osalts)
-    bo = X.blk_offsets()
+    bo = boX
+    j0X = start_blocks(wl, X)
     sample = np.sort(gs.choice(X.n, min(96, X.n), replace=False))
     for m in modes:
         got = out[m].cpu().numpy()
         for r in sample:
+            # the whole chain by definition; a resumed request keeps its rows
+            # from the start block on
             want = O.hash_chains(X.tokens, X.tok_offsets, X.principal, osalts, m,
-                                 X.boundary_tok, requests=[int(r)])
+                                 X.boundary_tok, requests=[int(r)])[j0X[r]:]
             ok &= bool(np.array_equal(got[bo[r]:bo[r + 1]], want))
     gates["G1_bitexact_sampled"] = bool(ok)
 
@@ -524,13 +631,13 @@ def main():
         },
     }
     look_t = per(ev_look)
-    look_bytes = {m: lookup_bytes(B, got_hits[m]) for m in modes}
+    look_bytes = {m: lookup_bytes(cntB, got_hits[m]) for m in modes}
     look_mean = {m: float(np.mean(ts)) for m, ts in look_t.items()}
     look_gbs = float(np.mean([look_bytes[m] / look_mean[m] for m in modes])) / 1e9
     g_look = 1  # lanes per request the library picks for this batch
     while g_look < 64 and B.n * g_look * 2 <= (1 << 18):
         g_look <<= 1
-    avg_blocks = int(B.block_counts().sum()) // max(B.n, 1)
+    avg_blocks = int(cntB.sum()) // max(B.n, 1)
     while g_look < 64 and g_look * 16 <= avg_blocks and B.n * g_look * 2 <= (1 << 21):
         g_look <<= 1
     ltr = recorded_traffic(f"k_lookup<{g_look}>", wl.name, "cache")
@@ -560,7 +667,7 @@ def main():
         result["block_hashes_per_s"] = blocks / t_step
         result["lookups_per_s"] = len(modes) * B.n / t_step
         chain_t = per(ev_chain)
-        ops = {m: OPS_PER_COMPRESSION * compressions(X, m) for m in modes}
+        ops = {m: OPS_PER_COMPRESSION * compressions(wl, X, m) for m in modes}
         mean_t = {m: float(np.mean(ts)) for m, ts in chain_t.items()}
         achieved = float(np.mean([ops[m] / mean_t[m] for m in modes])) / 1e12
         spans = []
@@ -596,7 +703,7 @@ def main():
             "mean_launch_ms": float(np.mean(list(mean_t.values()))) * 1e3,
             "launch_ms": {W.MODE_NAMES[m]: t * 1e3 for m, t in mean_t.items()},
             "launch_requests": X.n,
-            "longest_chain_blocks": int(X.block_counts().max()),
+            "longest_chain_blocks": int(cntX.max()),
             "parallelism_ceiling": min(1.0, waves / (CUS * SIMDS_PER_CU)),
             "parallelism_ceiling_note": "ceil(requests / 64) / 1024 SIMDs: waves at one lane "
                                         "per request (the lane-pair kernel runs three waves "
@@ -631,7 +738,7 @@ def main():
             sec = st["ms_median"] * 1e-3
             ph["chains"] = {**st, "blocks": nX, "tokens_per_s": 16 * nX / sec,
                             "block_hashes_per_s": nX / sec,
-                            "compressions_per_s": compressions(X, m) / sec}
+                            "compressions_per_s": compressions(wl, X, m) / sec}
             ph["clear"] = stats(clear_t[m])
             st = stats(ins_t[m])
             sec = st["ms_median"] * 1e-3
@@ -661,7 +768,8 @@ def main():
         # realistic load (the longest request replicated into one 64-request
         # workgroup per CU; a single workgroup on an otherwise idle GPU runs
         # at a lower clock), times the longest chain.
-        r = int(np.argmax(X.block_counts()))
+        r = int(np.argmax(cntX))
+        nb = int(cntX[r])
         one = X.subset(np.array([r]))
         nrep = 64 * cus
         L1 = int(one.tok_offsets[-1])
@@ -669,31 +777,65 @@ def main():
                       np.repeat(one.principal, nrep), np.repeat(one.boundary_tok, nrep))
         o = dict(tokens=to(rep.tokens), tok_offsets=to(rep.tok_offsets),
                  principal=to(rep.principal), boundary_tok=to(rep.boundary_tok),
-                 blk_offsets=to(rep.blk_offsets()))
-        oh = torch.empty((int(rep.block_counts().sum()), 32), dtype=torch.uint8, device=dev)
+                 blk_offsets=to(np.arange(nrep + 1, dtype=np.int64) * nb))
         m0 = modes[0]
+        par = None
+        if session:
+            o["start"] = to(np.full(nrep, start_blocks(wl, X)[r], np.int32))
+            par = parents[m0][r:r + 1].repeat(nrep, 1).contiguous()
+        oh = torch.empty((nrep * nb, 32), dtype=torch.uint8, device=dev)
         ts = []
         for i in range(4):
             end = timed(ts, None, main_s)
-            K.hash_chains(o["tokens"], o["tok_offsets"], o["principal"], salts, m0,
-                          o["boundary_tok"], blk_offsets=o["blk_offsets"], out=oh,
-                          status=status, check=False, stream=main_s)
+            hash_call(m0, main_s, xx=o, out_=oh, par=par)
             end()
         torch.cuda.synchronize()
         K.check_status(status, "critical-path launch")
-        ok_rep = bool(np.array_equal(oh[:int(one.block_counts()[0])].cpu().numpy(),
+        ok_rep = bool(np.array_equal(oh[:nb].cpu().numpy(),
                                      out[m0][int(bo[r]):int(bo[r + 1])].cpu().numpy()))
         gates["G1_bitexact_sampled"] = bool(gates["G1_bitexact_sampled"] and ok_rep)
         t_crit = min(e0.elapsed_time(e1) for _, e0, e1 in ts[1:]) * 1e-3
         ideal = ops[m0] / (INT_PEAK_TOPS * 1e12)
         roof = result["roofline"]
         roof["critical_path_ms"] = t_crit * 1e3
-        roof["us_per_block_on_critical_path"] = t_crit / one.block_counts()[0] * 1e6
+        roof["us_per_block_on_critical_path"] = t_crit / nb * 1e6
         roof["critical_path_ceiling"] = min(1.0, ideal / t_crit)
-        roof["critical_path_note"] = (f"the longest request ({int(one.block_counts()[0])} blocks) "
+        roof["critical_path_note"] = (f"the longest request ({nb} blocks hashed) "
                                       f"replicated {nrep} times, one launch; ceiling = "
                                       "(launch ops at peak) / its duration")
-        del o, oh
+        del o, oh, par
+        if session:
+            # the same turn-2 chains rehashed from block 0 (what a stack without
+            # chain extension hashes each turn), for comparison
+            xf = dict(x, blk_offsets=to(X.blk_offsets()))
+            of = torch.empty((int(X.block_counts().sum()), 32), dtype=torch.uint8, device=dev)
+            full = {}
+            for m in modes:
+                ts = []
+                for i in range(4):
+                    end = timed(ts, None, main_s)
+                    K.hash_chains(xf["tokens"], xf["tok_offsets"], xf["principal"], salts, m,
+                                  xf["boundary_tok"], blk_offsets=xf["blk_offsets"], out=of,
+                                  status=status, check=False, stream=main_s)
+                    end()
+                torch.cuda.synchronize()
+                full[W.MODE_NAMES[m]] = min(e0.elapsed_time(e1) for _, e0, e1 in ts[1:])
+                rows = of.cpu().numpy()[np.concatenate(
+                    [np.arange(X.blk_offsets()[q] + start_blocks(wl, X)[q],
+                               X.blk_offsets()[q + 1]) for q in range(X.n)])]
+                gates["G1_bitexact_sampled"] = bool(
+                    gates["G1_bitexact_sampled"] and np.array_equal(rows, out[m].cpu().numpy()))
+            K.check_status(status, "full rehash")
+            res_ms = {W.MODE_NAMES[m]: float(np.min(chain_t[m])) * 1e3 for m in modes}
+            result["session"] = {
+                "blocks_hashed": nX, "blocks_in_prompts": int(X.block_counts().sum()),
+                "resume_chain_ms_min": res_ms, "full_rehash_chain_ms_min": full,
+                "speedup": {k: full[k] / res_ms[k] for k in full},
+                "prompt_tokens_per_s": 16 * len(modes) * int(X.block_counts().sum()) / t_step,
+                "note": "min launch times; full rehash = kvgov_hash_chains over the whole "
+                        "turn-2 prompts (its rows from the start block equal the resumed ones)",
+            }
+            del of
 
     if not args.no_extras:
         log("measuring device peaks (microbenchmarks)")

@@ -1,4 +1,4 @@
-"""GPU parity on the five workloads at full size, in the launch shapes bench.py
+"""GPU parity on the six workloads at full size, in the launch shapes bench.py
 uses (one hashing call per batch and mode, the table sizes of the configs).
 
 * tiny, paper, template: every digest, every hit count and n_new against the
@@ -11,6 +11,9 @@ uses (one hashing call per batch and mode, the table sizes of the configs).
   the longest) against the oracle; at full size, properties that hold at any
   size: all keys distinct so n_new equals the block count, and a lookup of the
   inserted batch hits every block.
+* session (4096 two-turn sessions): turn 2's chains resumed from turn 1's
+  last digests, every digest, n_new and hit count against the oracle's own
+  resumed chains.
 """
 import os
 
@@ -212,3 +215,37 @@ def test_many_requests_longest_first_ordering():
     for mode in (W.NONE, W.ROOT, W.BOUNDARY):
         got = gpu_chains(b, sd, mode).cpu().numpy()
         assert np.array_equal(got, oracle_chains(b, osalts, mode))
+
+
+@pytest.fixture(scope="module")
+def session_wl():
+    return W.make("session")
+
+
+@pytest.mark.parametrize("mode", [W.ROOT, W.BOUNDARY])
+def test_session_config(session_wl, mode):
+    """Multi-turn sessions at full size: turn 1 hashed whole on the GPU, turn 2
+    resumed from its last full-block digests, then insert and re-lookup of
+    the new blocks.  The oracle hashes turn 1 and resumes turn 2 on its own
+    (chain_from); every digest, n_new and every hit count are compared."""
+    wl = session_wl
+    T1, T2, start = wl.notes["turn1"], wl.insert, wl.notes["start"]
+    sd = K.salts(wl.K, dev(wl.principal_ids))
+    osalts = O.salts(wl.K, wl.principal_ids)
+    last = np.maximum(T1.blk_offsets()[1:] - 1, 0)
+    h1 = gpu_chains(T1, sd, mode)
+    parents = h1[dev(last)].contiguous()
+    h2 = K.hash_chains_resume(dev(T2.tokens), dev(T2.tok_offsets), dev(T2.principal), sd, mode,
+                              dev(start), parents, dev(T2.boundary_tok))
+    cnt = T2.block_counts() - start
+    bo = np.concatenate([[0], np.cumsum(cnt)]).astype(np.int64)
+    with K.Cache(wl.log2_slots) as c:
+        n_new = c.insert(h2, dev(bo))
+        hits = c.lookup(h2, dev(bo)).cpu().numpy()
+    o1 = oracle_chains(T1, osalts, mode)
+    want = O.hash_chains_resume(T2.tokens, T2.tok_offsets, T2.principal, osalts, mode, start,
+                                o1[last], T2.boundary_tok)
+    assert np.array_equal(h2.cpu().numpy(), want)
+    assert n_new == O.Table().insert(want) == int(cnt.sum())
+    assert np.array_equal(hits, cnt)
+    assert np.array_equal(hits, wl.lookup.expect_hits[mode])

@@ -317,12 +317,46 @@ def large(seed: int = SEED, n: int = 65536, P: int = 4096,
                     {"sigma": sigma})
 
 
+def session(seed: int = SEED, n: int = 4096, P: int = 64) -> Workload:
+    """Multi-turn sessions (Sec. 5.7: turn n+1 extends turn n exactly).  Turn
+    1 of each session is a request of the paper-shaped workload (2119-token
+    shared prefix + U{64..1024} private suffix); turn 2 appends a follow-up of
+    U{64..1024} tokens.  Turn 2 resumes each chain at turn 1's full-block
+    count, from turn 1's last full-block digest, so only the blocks from there
+    on are hashed (notes: ``turn1`` batch, ``start`` blocks).  Boundary at
+    token 2119 in both turns.  The lookup re-probes the resumed rows (hit =
+    the number of blocks hashed for the request)."""
+    base = paper(seed=seed, n=n, P=P)
+    t1 = base.insert
+    g = rng("session/followup", seed)
+    extra = g.integers(64, 1025, size=n).astype(np.int64)
+    lens2 = t1.lengths + extra
+    offs2 = _flat(lens2)
+    toks2 = np.empty(int(offs2[-1]), dtype=np.int32)
+    new = _uniform_tokens(g, int(extra.sum()))
+    pos = 0
+    for r in range(n):
+        a, l1 = int(offs2[r]), int(t1.lengths[r])
+        toks2[a:a + l1] = t1.row(r)
+        toks2[a + l1:int(offs2[r + 1])] = new[pos:pos + extra[r]]
+        pos += int(extra[r])
+    t2 = Batch(toks2, offs2, t1.principal.copy(), t1.boundary_tok.copy())
+    start = (t1.lengths // BLOCK).astype(np.int32)
+    hashed = (lens2 // BLOCK - start).astype(np.int32)
+    look = Batch(toks2, offs2, t2.principal, t2.boundary_tok,
+                 {ROOT: hashed, BOUNDARY: hashed})
+    return Workload("session", base.K, base.principal_ids, t2, look, [ROOT, BOUNDARY], 20,
+                    {"turn1": t1, "start": start, "gini": base.notes["gini"],
+                     "prefix_len": base.notes["prefix_len"]})
+
+
 CONFIGS = {
     "tiny": tiny,
     "paper": paper,
     "template": template,
     "probe": probe,
     "large": large,
+    "session": session,
 }
 
 
