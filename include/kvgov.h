@@ -35,8 +35,9 @@
  *   - K and the salts are secrets: the library keeps no copy of K after
  *     kvgov_salts returns and logs nothing.
  *   - The calls allocate no device memory except kvgov_cache_create and the
- *     stream-ordered scratch of kvgov_hash_chains and its resume variant
- *     (see there) and of the offset helpers (8 bytes per 1024 requests).
+ *     stream-ordered scratch of kvgov_hash_chains and its resume variant,
+ *     of kvgov_cache_admit (see there) and of the offset helpers (8 bytes
+ *     per 1024 requests).
  */
 #ifndef KVGOV_H
 #define KVGOV_H
@@ -236,6 +237,34 @@ int kvgov_cache_insert(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
  */
 int kvgov_cache_lookup(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,
                        int32_t n, int64_t n_blocks, int32_t *hit_blocks, void *stream);
+
+/*
+ * Admission: lookup-then-insert for a batch in one call, as a serving
+ * engine's scheduler admits requests one after another (Sec. 2.1: a request
+ * reuses the longest cached block prefix and the blocks it computes join the
+ * cache).  Requests are taken in order r = 0 .. n-1; request r sees
+ *   V_r = T  u  {every key of requests 0 .. r-1}
+ * (T = the table before the call), and
+ *   hit_blocks[r] = the first j whose key is not in V_r (or the row count),
+ *   new_blocks[r] = the number of distinct keys of request r not in V_r,
+ * and afterwards T <- T u {every key of the batch}.  Sum of new_blocks =
+ * the keys the call added.  The result does not depend on how the work is
+ * scheduled on the device.
+ *
+ * hashes, blk_offsets, n, n_blocks as for kvgov_cache_insert.
+ * hit_blocks, new_blocks  device out, int32 [n].
+ * n_new        host out or NULL, as for kvgov_cache_insert.
+ * Scratch: 4 * n_blocks bytes from hipMallocAsync on `stream`, freed in
+ * stream order.
+ * Kernel errors: KVGOV_E_OFFSETS (latched; outputs of the batch are not
+ * meaningful, rows of requests found malformed are set to 0), KVGOV_E_FULL
+ * (latched; keys that found no slot count as not visible and not new).
+ * Errors: KVGOV_E_INVAL, KVGOV_E_NOMEM, KVGOV_E_UNSUPPORTED (2^32 - 1
+ * insert or admit calls since the last clear), KVGOV_E_HIP.
+ */
+int kvgov_cache_admit(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,
+                      int32_t n, int64_t n_blocks, int32_t *hit_blocks, int32_t *new_blocks,
+                      int64_t *n_new, void *stream);
 
 /* Waits for `stream`; stores the number of keys in T and returns the latched
  * error, if any. */

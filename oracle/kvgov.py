@@ -242,6 +242,25 @@ class Table:
         """hit[r] = first j with h_j(r) not in T, or n_full(r) if none is missing."""
         return lookup_hits(self.keys, hashes, blk_offsets)
 
+    def admit(self, hashes: np.ndarray, blk_offsets):
+        """Requests in order, each looked up and then inserted (Sec. 2.1: a
+        request reuses the longest cached block prefix, and the blocks it
+        computes join the cache).  Returns (hits, new): hits[r] as ``lookup``
+        against T as it stands when r comes, new[r] = distinct keys of r
+        not yet in T; T then takes r's keys."""
+        blk_offsets = np.asarray(blk_offsets, dtype=np.int64)
+        n = blk_offsets.shape[0] - 1
+        hits = np.zeros(n, dtype=np.int32)
+        new = np.zeros(n, dtype=np.int32)
+        for r in range(n):
+            a, b = int(blk_offsets[r]), int(blk_offsets[r + 1])
+            keys_r = _keys(hashes, a, b)
+            hits[r] = lookup_hits(self.keys, hashes, blk_offsets, requests=[r])[0]
+            fresh = set(keys_r) - self.keys
+            new[r] = len(fresh)
+            self.keys |= fresh
+        return hits, new
+
 
 def lookup_hits(keys: set, hashes: np.ndarray, blk_offsets,
                 requests: Optional[Iterable[int]] = None) -> np.ndarray:

@@ -14,8 +14,8 @@
 //                       insert call that claimed the slot and the index of the
 //                       claiming key within that call's input.
 //   meta                key count, per-call counters, latched error, and the
-//                       presence bit of the all-0xFF key, which cannot live in
-//                       a slot because it is the empty pattern.
+//                       tag and presence bit of the all-0xFF key, which cannot
+//                       live in a slot because it is the empty pattern.
 //
 // Insert protocol (no fences, no waiting on other lanes).  A key walks its
 // probe sequence; at each slot it reads the tag:
@@ -29,6 +29,14 @@
 // Equal -> already present, stop.  Otherwise move to the next slot.  Two
 // copies of one key follow the same sequence and each slot changes state at
 // most once, so exactly one copy claims a slot and the other finds it.
+//
+// Admission (lookup-then-insert in request order) runs the same insert and
+// additionally lowers a slot claimed in the call to the smallest claiming
+// row (atomicMin on the tag: the epoch bits are equal, so the minimum is the
+// earliest row, i.e. the earliest request holding the key), and records per
+// row which slot its key went to; a second kernel then decides per request
+// what it sees: keys of earlier calls, and keys whose earliest row lies in an
+// earlier request.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -50,6 +58,7 @@ struct CacheMeta {
   unsigned long long n_keys[kCounterLanes];       // keys in the table (all-0xFF key included)
   unsigned long long new_keys[2][kCounterLanes];  // keys added by insert call `epoch`, at [epoch & 1]
   unsigned long long exported;                    // keys written by the latest export
+  unsigned long long ones_tag;                    // the all-0xFF key's tag (0 = absent)
   int32_t status;                                 // latched error (0 = none)
   int32_t ones_present;                           // the all-0xFF key is in the table
 };
@@ -111,6 +120,7 @@ __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long l
     }
     if (threadIdx.x == 0) {
       m->exported = 0;
+      m->ones_tag = 0;
       m->status = 0;
       m->ones_present = 0;
     }
@@ -131,16 +141,41 @@ __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t *lds4) {
   return threadIdx.x == 0 ? lds4[0] + lds4[1] + lds4[2] + lds4[3] : 0;
 }
 
-// Tags only ever change from 0 to a claim, so a plain (possibly stale) read
-// can only show 0 for a claimed slot; the compare-and-swap that follows then
-// fails and returns the claim.  Coherent atomics are used for the claim only.
-// Returns 1 if the key was added.
+// Per-row codes written by the admission insert: the slot of the row's key,
+// or one of these (slots < 2^31, so no slot index collides with them).
+constexpr uint32_t kCodeOnes = 0xFFFFFFFEu;    // the all-0xFF key (tag in meta)
+constexpr uint32_t kCodeDup = 0xFFFFFFFDu;     // equals the previous request's key here
+constexpr uint32_t kCodeFailed = 0xFFFFFFFCu;  // not inserted (table full)
+
+// A tag claimed in this call (same epoch) whose row is above `mine`: lower
+// it.  Reads first, so most copies of a hot key issue no atomic.
+__device__ __forceinline__ void lower_claim(unsigned long long *tag, unsigned long long seen,
+                                            unsigned long long mine) {
+  if (mine < seen) atomicMin(tag, mine);
+}
+
+// Tags only ever change from 0 to a claim (and, within the claiming call, to
+// a smaller claim of the same key), so a plain (possibly stale) read can only
+// show 0 for a claimed slot; the compare-and-swap that follows then fails
+// and returns the claim.  Coherent atomics are used for the claim only.
+// Returns 1 if the key was added; *code receives where the key went.
+template <bool ADMIT>
 __device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &key, int64_t i,
                                                int64_t lo, const uint8_t *hashes,
-                                               uint32_t epoch) {
-  if (key_is_empty_pattern(key)) return atomicExch(&t.meta->ones_present, 1) == 0 ? 1u : 0u;
+                                               uint32_t epoch, uint32_t *code) {
   const unsigned long long mine = ((unsigned long long)epoch << 32) |
                                   (unsigned long long)(i - lo + 1);
+  if (key_is_empty_pattern(key)) {
+    *code = kCodeOnes;
+    unsigned long long expect = 0;
+    if (__hip_atomic_compare_exchange_strong(&t.meta->ones_tag, &expect, mine, __ATOMIC_RELAXED,
+                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+      atomicExch(&t.meta->ones_present, 1);
+      return 1;
+    }
+    if (ADMIT && (uint32_t)(expect >> 32) == epoch) lower_claim(&t.meta->ones_tag, expect, mine);
+    return 0;
+  }
   uint64_t s = slot_hash(key) & t.mask;
   for (uint64_t probes = 0; probes <= t.mask; ++probes) {
     unsigned long long tag = t.tags[s];
@@ -150,21 +185,28 @@ __device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &ke
                                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
         t.keys[2 * s] = key.lo;
         t.keys[2 * s + 1] = key.hi;
+        *code = (uint32_t)s;
         return 1;
       }
       tag = expect;  // somebody claimed it first: examine the claimant
     }
     Key other;
-    if ((uint32_t)(tag >> 32) == epoch) {
+    const bool current = (uint32_t)(tag >> 32) == epoch;
+    if (current) {
       const int64_t c = (int64_t)(tag & 0xFFFFFFFFull) - 1;
       other = load_key(hashes + (lo + c) * 32);
     } else {
       other = Key{t.keys[2 * s], t.keys[2 * s + 1]};
     }
-    if (key_eq(key, other)) return 0;
+    if (key_eq(key, other)) {
+      if (ADMIT && current) lower_claim(&t.tags[s], tag, mine);
+      *code = (uint32_t)s;
+      return 0;
+    }
     s = (s + 1) & t.mask;
   }
   atomicCAS(&t.meta->status, 0, KVGOV_E_FULL);
+  *code = kCodeFailed;
   return 0;
 }
 
@@ -197,9 +239,16 @@ __device__ __forceinline__ int32_t find_request(const int64_t *bo, int32_t n, in
 // one), and the compared position is checked to lie in the batch, so
 // malformed interior offsets cannot cause a wrong result or an
 // out-of-range read.
+//
+// ADMIT: also the admission's first half: claims are lowered to the
+// earliest row, and codes[f] records where row f's key went (kCodeDup for a
+// key skipped as equal to the previous request's, which is in an earlier
+// request by construction).
+template <bool ADMIT>
 __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hashes,
                                                 const int64_t *blk_offsets, int32_t n,
-                                                int64_t n_blocks, uint32_t epoch) {
+                                                int64_t n_blocks, uint32_t epoch,
+                                                uint32_t *codes) {
   __shared__ uint32_t lds4[4];
   const int64_t lo = blk_offsets[0], hi = blk_offsets[n];
   const bool first = blockIdx.x == 0 && threadIdx.x == 0;
@@ -239,7 +288,9 @@ __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hash
         const int64_t jj = f - b_r;
         if (r >= 1 && jj >= 0 && jj < b_r - b_p && b_p + jj >= lo)
           dup = key_eq(key, load_key(hashes + (b_p + jj) * 32));
-        if (!dup) added += insert_key(t, key, f, lo, hashes, epoch);
+        uint32_t code = kCodeDup;
+        if (!dup) added += insert_key<ADMIT>(t, key, f, lo, hashes, epoch, &code);
+        if (ADMIT) codes[f] = code;
       }
       rc = __shfl(r, 63, 64);
     }
@@ -338,6 +389,80 @@ __global__ __launch_bounds__(256) void k_lookup(LookupArgs a) {
   if (sub == 0) a.hit_blocks[r] = (int32_t)hit;
 }
 
+struct AdmitArgs {
+  TableView t;
+  const int64_t *blk_offsets;
+  int32_t n;
+  int64_t n_blocks;
+  uint32_t epoch;
+  const uint32_t *codes;  // per row, from k_insert<true>
+  int32_t *hit_blocks;
+  int32_t *new_blocks;
+};
+
+// Second half of the admission: G lanes per request walk all of its rows G
+// at a time.  Row f of request r (rows [b0, b1)) with key K:
+//   visible to r  <=>  K was in the table before the call (a tag of an
+//                      earlier epoch), or K's earliest row in the call lies
+//                      before b0 (an earlier request holds it);
+//   new for r     <=>  K's earliest row is f itself.
+// hit_blocks[r] = first row not visible (relative to b0), new_blocks[r] =
+// rows new for r.  The earliest rows are final: k_insert<true> has ended.
+template <int G>
+__global__ __launch_bounds__(256) void k_admit_scan(AdmitArgs a) {
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t r = gid / G;
+  if (r >= a.n) return;  // groups never straddle this test: 256 % G == 0
+  const int sub = (int)(gid % G);
+  const int lane = threadIdx.x & 63;
+  const int base = lane & ~(G - 1);
+  const uint64_t gmask = (G == 64) ? ~0ull : (((1ull << G) - 1ull) << base);
+  const int64_t lo = a.blk_offsets[0], hi = a.blk_offsets[a.n];
+  const int64_t b0 = a.blk_offsets[r], b1 = a.blk_offsets[r + 1];
+  // the batch check of k_insert (which then wrote no codes), and this
+  // request's rows inside the batch
+  if (lo < 0 || hi < lo || hi > a.n_blocks || hi - lo >= 0xFFFFFFFFll || b0 < lo || b1 < b0 ||
+      b1 > hi) {
+    if (sub == 0) {
+      atomicCAS(&a.t.meta->status, 0, KVGOV_E_OFFSETS);
+      a.hit_blocks[r] = 0;
+      a.new_blocks[r] = 0;
+    }
+    return;
+  }
+  const int64_t nf = b1 - b0;
+  int64_t hit = nf;
+  uint32_t fresh = 0;
+  for (int64_t j0 = 0; j0 < nf; j0 += G) {
+    const int64_t j = j0 + sub;
+    bool seen = true;
+    if (j < nf) {
+      const int64_t f = b0 + j;
+      const uint32_t code = a.codes[f];
+      if (code == kCodeFailed) {
+        seen = false;
+      } else if (code != kCodeDup) {
+        const unsigned long long tag =
+            code == kCodeOnes ? a.t.meta->ones_tag : a.t.tags[code];
+        if ((uint32_t)(tag >> 32) == a.epoch) {
+          const int64_t first = lo + (int64_t)(tag & 0xFFFFFFFFull) - 1;
+          seen = first < b0;
+          fresh += first == f ? 1u : 0u;
+        }
+      }
+    }
+    const uint64_t m = __ballot(!seen) & gmask;
+    if (m && hit == nf) hit = j0 + (__builtin_ctzll(m) - base);
+  }
+  // sum of `fresh` over the group
+#pragma unroll
+  for (int d = G / 2; d >= 1; d >>= 1) fresh += __shfl_xor(fresh, d, 64);
+  if (sub == 0) {
+    a.hit_blocks[r] = (int32_t)hit;
+    a.new_blocks[r] = (int32_t)fresh;
+  }
+}
+
 __global__ void k_export_begin(CacheMeta *m) { m->exported = 0; }
 
 // One atomic per wave reserves the output rows of the wave's keys.
@@ -413,12 +538,30 @@ int enqueue_clear(kvgov_cache *c, hipStream_t s) {
   return launch_status();
 }
 
+// Waves of 4 x kInsChunk keys, at most 16 workgroups per CU.
+unsigned insert_grid(int64_t n_blocks) {
+  const int64_t groups = ceil_div(std::max<int64_t>(n_blocks, 1), (int64_t)kInsChunk * 4);
+  return (unsigned)std::min<int64_t>(groups, (int64_t)device_cu_count() * 16);
+}
+
 int read_meta(kvgov_cache *c, CacheMeta *m, hipStream_t s) {
   if (hipMemcpyAsync(m, c->view.meta, sizeof(CacheMeta), hipMemcpyDeviceToHost, s) !=
       hipSuccess)
     return KVGOV_E_HIP;
   if (hipStreamSynchronize(s) != hipSuccess) return KVGOV_E_HIP;
   return KVGOV_OK;
+}
+
+// Keys added by insert call `epoch` (waits for the stream), and the latched
+// error.
+int read_new_keys(kvgov_cache *c, uint32_t epoch, int64_t *n_new, hipStream_t s) {
+  CacheMeta m{};
+  int rc = read_meta(c, &m, s);
+  if (rc != KVGOV_OK) return rc;
+  int64_t added = 0;
+  for (int i = 0; i < kCounterLanes; ++i) added += (int64_t)m.new_keys[epoch & 1][i];
+  *n_new = added;
+  return m.status;
 }
 
 }  // namespace
@@ -495,20 +638,11 @@ int kvgov_cache_insert(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
   hipStream_t s = as_stream(stream);
   uint32_t epoch = c->epoch.fetch_add(1) + 1;
   if (epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;  // 2^32 - 1 inserts since clear
-  const int64_t ins_groups = ceil_div(std::max<int64_t>(n_blocks, 1), (int64_t)kInsChunk * 4);
-  const unsigned ins_grid =
-      (unsigned)std::min<int64_t>(ins_groups, (int64_t)device_cu_count() * 16);
-  hipLaunchKernelGGL(k_insert, dim3(ins_grid), dim3(256), 0, s, c->view, hashes,
-                     blk_offsets, n, n_blocks, epoch);
+  hipLaunchKernelGGL(k_insert<false>, dim3(insert_grid(n_blocks)), dim3(256), 0, s, c->view,
+                     hashes, blk_offsets, n, n_blocks, epoch, nullptr);
   rc = launch_status();
   if (rc != KVGOV_OK || !n_new) return rc;
-  CacheMeta m{};
-  rc = read_meta(c, &m, s);
-  if (rc != KVGOV_OK) return rc;
-  int64_t added = 0;
-  for (int i = 0; i < kCounterLanes; ++i) added += (int64_t)m.new_keys[epoch & 1][i];
-  *n_new = added;
-  return m.status;
+  return read_new_keys(c, epoch, n_new, s);
 }
 
 // Lanes per request for lookup: enough groups in flight to cover the chip
@@ -548,6 +682,56 @@ int kvgov_cache_lookup(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
     default: hipLaunchKernelGGL(k_lookup<64>, grid, block, 0, s, a); break;
   }
   return launch_status();
+}
+
+// Lanes per request for the admission scan, which walks every row of a
+// request: about one lane per 2 rows of the average request, 4 to 64.
+static int admit_group(int32_t n, int64_t n_blocks) {
+  const int64_t avg = n > 0 ? n_blocks / n : 0;
+  int g = 4;
+  while (g < 64 && (int64_t)g * 2 < avg) g <<= 1;
+  return g;
+}
+
+int kvgov_cache_admit(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,
+                      int32_t n, int64_t n_blocks, int32_t *hit_blocks, int32_t *new_blocks,
+                      int64_t *n_new, void *stream) {
+  if (!c || !blk_offsets || n < 0 || n_blocks < 0 || (n_blocks > 0 && !hashes) ||
+      (n > 0 && (!hit_blocks || !new_blocks)))
+    return KVGOV_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(hashes) & 3) return KVGOV_E_INVAL;
+  int rc = check_device(c);
+  if (rc != KVGOV_OK) return rc;
+  if (n == 0) {
+    if (n_new) *n_new = 0;
+    return KVGOV_OK;
+  }
+  hipStream_t s = as_stream(stream);
+  uint32_t *codes = nullptr;
+  if (hipMallocAsync(reinterpret_cast<void **>(&codes),
+                     sizeof(uint32_t) * (size_t)std::max<int64_t>(n_blocks, 1), s) != hipSuccess)
+    return KVGOV_E_NOMEM;
+  const uint32_t epoch = c->epoch.fetch_add(1) + 1;
+  if (epoch == 0xFFFFFFFFu) {
+    (void)hipFreeAsync(codes, s);
+    return KVGOV_E_UNSUPPORTED;
+  }
+  hipLaunchKernelGGL(k_insert<true>, dim3(insert_grid(n_blocks)), dim3(256), 0, s, c->view,
+                     hashes, blk_offsets, n, n_blocks, epoch, codes);
+  AdmitArgs a{c->view, blk_offsets, n, n_blocks, epoch, codes, hit_blocks, new_blocks};
+  const int g = admit_group(n, n_blocks);
+  const dim3 grid((unsigned)ceil_div((int64_t)n * g, 256)), block(256);
+  switch (g) {
+    case 4: hipLaunchKernelGGL(k_admit_scan<4>, grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL(k_admit_scan<8>, grid, block, 0, s, a); break;
+    case 16: hipLaunchKernelGGL(k_admit_scan<16>, grid, block, 0, s, a); break;
+    case 32: hipLaunchKernelGGL(k_admit_scan<32>, grid, block, 0, s, a); break;
+    default: hipLaunchKernelGGL(k_admit_scan<64>, grid, block, 0, s, a); break;
+  }
+  rc = launch_status();
+  if (hipFreeAsync(codes, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
+  if (rc != KVGOV_OK || !n_new) return rc;
+  return read_new_keys(c, epoch, n_new, s);
 }
 
 int kvgov_cache_count(kvgov_cache *c, int64_t *n_keys, void *stream) {

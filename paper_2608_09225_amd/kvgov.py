@@ -13,7 +13,7 @@ Calls mirror the C ABI one to one:
     kvgov_hash_chains   -> hash_chains(tokens, tok_offsets, principal, salts, mode, ...)
     kvgov_hash_chains_resume -> hash_chains_resume(..., start_block, parents, ...)
     kvgov_resume_offsets -> resume_offsets(tok_offsets, start_block)
-    kvgov_cache_*       -> Cache(log2_slots).insert / lookup / clear / count / export
+    kvgov_cache_*       -> Cache(log2_slots).insert / lookup / admit / clear / count / export
 """
 from __future__ import annotations
 
@@ -52,6 +52,8 @@ _SIGNATURES = {
     "kvgov_cache_insert": (ctypes.c_int, [_vp, _vp, _vp, _c_i32, _c_i64,
                                           ctypes.POINTER(_c_i64), _vp]),
     "kvgov_cache_lookup": (ctypes.c_int, [_vp, _vp, _vp, _c_i32, _c_i64, _vp, _vp]),
+    "kvgov_cache_admit": (ctypes.c_int, [_vp, _vp, _vp, _c_i32, _c_i64, _vp, _vp,
+                                         ctypes.POINTER(_c_i64), _vp]),
     "kvgov_cache_count": (ctypes.c_int, [_vp, ctypes.POINTER(_c_i64), _vp]),
     "kvgov_cache_export": (ctypes.c_int, [_vp, _vp, _c_i64, ctypes.POINTER(_c_i64), _vp]),
 }
@@ -322,6 +324,27 @@ class Cache:
                                         hs.shape[0] if hs.dim() else 0, _ptr(out),
                                         _stream(stream)), "kvgov_cache_lookup")
         return out
+
+    def admit(self, hashes: torch.Tensor, blk_offsets: torch.Tensor, sync: bool = True,
+              hits: Optional[torch.Tensor] = None, new: Optional[torch.Tensor] = None,
+              stream=None):
+        """Lookup-then-insert in request order: (hit_blocks, new_blocks, n_new);
+        n_new is None unless ``sync``."""
+        hs = _dev(hashes, torch.uint8, "hashes")
+        bo = _dev(blk_offsets, torch.int64, "blk_offsets")
+        n = bo.numel() - 1
+        if hits is None:
+            hits = torch.empty(n, dtype=torch.int32, device=bo.device)
+        if new is None:
+            new = torch.empty(n, dtype=torch.int32, device=bo.device)
+        _dev(hits, torch.int32, "hits")
+        _dev(new, torch.int32, "new")
+        nn = _c_i64(-1)
+        _check(lib().kvgov_cache_admit(self.handle, _ptr(hs), _ptr(bo), n,
+                                       hs.shape[0] if hs.dim() else 0, _ptr(hits), _ptr(new),
+                                       ctypes.byref(nn) if sync else None, _stream(stream)),
+               "kvgov_cache_admit")
+        return hits, new, (int(nn.value) if sync else None)
 
     def count(self, stream=None) -> int:
         v = _c_i64()

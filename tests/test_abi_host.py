@@ -117,6 +117,7 @@ def test_host_validation_returns_before_any_launch():
     n = ctypes.c_int64()
     assert L.kvgov_cache_insert(None, fake, fake, 1, 4, None, None) == INVAL
     assert L.kvgov_cache_lookup(None, fake, fake, 1, 4, fake, None) == INVAL
+    assert L.kvgov_cache_admit(None, fake, fake, 1, 4, fake, fake, None, None) == INVAL
     assert L.kvgov_cache_clear(None, None) == INVAL
     assert L.kvgov_cache_count(None, ctypes.byref(n), None) == INVAL
     assert L.kvgov_cache_export(None, fake, 1, ctypes.byref(n), None) == INVAL
