@@ -27,10 +27,12 @@ longest request hashed alone), the device's measured peaks (integer-VALU and
 those, and the CPU oracle per phase, on one core and with the host's CPU
 model and SHA extension flag.
 
---config {tiny,template,large,session} runs the same kind of step on those
-workloads (large: chains + insert + a re-lookup of the inserted batch;
-session: turn-2 chains resumed at turn 1's last full block from its digest,
-insert and re-lookup of the new blocks, and the full rehash timed beside);
+--config {tiny,template,large,session,admission} runs the same kind of step
+on those workloads (large: chains + insert + a re-lookup of the inserted
+batch; session: turn-2 chains resumed at turn 1's last full block from its
+digest, insert and re-lookup of the new blocks, and the full rehash timed
+beside; admission: the paper-shaped chains, then one lookup-then-insert
+call over both batches in request order instead of insert + lookup);
 --config probe times lookups alone against the 8M-key resident table (the
 resident chains, the probe chains and the insert are done before timing).
 Only the default is the bench line; the others are for the per-config table.
@@ -76,6 +78,11 @@ LOOKUP_BYTES_PER_REQUEST = 20
 # a key already present reads the query and the slot holding it.
 INSERT_BYTES_NEW = 96
 INSERT_BYTES_PRESENT = 64
+# Admission: the insert's bytes, plus per row a 4-byte code written and read
+# back and an 8-byte tag read; per request two 8-byte offsets and two 4-byte
+# outputs.
+ADMIT_BYTES_PER_ROW = 16
+ADMIT_BYTES_PER_REQUEST = 24
 
 DESCRIPTIONS = {
     "paper": "paper-shaped shared prefix: 4096 requests x 2 batches (insert, re-lookup with "
@@ -88,6 +95,9 @@ DESCRIPTIONS = {
              "1M probes of U{{8..64}} blocks, 70% own-principal prefixes, 30% foreign",
     "large": "large batch: 65536 requests, lognormal lengths (median 2048, sigma 1, max "
              "32768 tokens), 4096 principals, root and boundary; chains + insert + re-lookup",
+    "admission": "paper-shaped batches admitted in order: 8192 requests (4096 insert-batch "
+                 "then 4096 re-lookup-batch), 64 principals, root and boundary (token 2119); "
+                 "chains + one lookup-then-insert call per mode",
     "session": "multi-turn sessions: 4096 turn-2 prompts (paper-shaped turn 1 + U{{64..1024}} "
                "follow-up tokens), 64 principals, root and boundary (token 2119); chains "
                "resumed at turn 1's last full block + insert + re-lookup of the new blocks",
@@ -159,6 +169,21 @@ def compressions(wl: W.Workload, batch: W.Batch, mode: int) -> int:
     return c
 
 
+def admit_bytes(n_req: int, rows: int, n_new: int) -> int:
+    """Algorithmic bytes of one admission call (both kernels)."""
+    return (INSERT_BYTES_NEW * n_new + INSERT_BYTES_PRESENT * (rows - n_new) +
+            ADMIT_BYTES_PER_ROW * rows + ADMIT_BYTES_PER_REQUEST * n_req)
+
+
+def admit_group(n: int, rows: int) -> int:
+    """Lanes per request of the admission scan (the library's rule)."""
+    avg = rows // n if n else 0
+    g = 4
+    while g < 64 and g * 2 < avg:
+        g <<= 1
+    return g
+
+
 def lookup_bytes(counts: np.ndarray, hits: np.ndarray) -> int:
     examined = np.minimum(hits.astype(np.int64) + 1, counts)
     return int(examined.sum()) * LOOKUP_BYTES_PER_BLOCK + counts.size * LOOKUP_BYTES_PER_REQUEST
@@ -214,6 +239,8 @@ def cpu_baseline(wl: W.Workload, processes: int, max_blocks: int):
         return cpu_baseline_probe(wl, processes)
     if wl.name == "session":
         return cpu_baseline_session(wl, processes)
+    if wl.name == "admission":
+        return cpu_baseline_admission(wl, processes)
     same = wl.name == "large"
     A = capped(wl.insert, max_blocks)
     B = A if same else capped(wl.lookup, max_blocks)
@@ -269,6 +296,44 @@ def cpu_baseline(wl: W.Workload, processes: int, max_blocks: int):
                 "sample": f"chains of the first {one.n} insert requests, "
                           f"{W.MODE_NAMES[wl.modes[0]]} mode",
                 "salts_us_per_key": cpu_salt_cost(wl) * 1e6,
+            },
+            "host": host_cpu_info()}
+
+
+def cpu_baseline_admission(wl: W.Workload, processes: int):
+    """The oracle's chains of both batches (over worker processes), then its
+    admission (one process) of the 2n requests in order."""
+    import oracle as O
+    X = concat(wl.insert, wl.lookup)
+    clock = time.perf_counter
+    t = {"salts": 0.0, "chains": 0.0, "admit": 0.0}
+    t0 = clock()
+    salts = O.salts(wl.K, wl.principal_ids)
+    t["salts"] = clock() - t0
+    bo = X.blk_offsets()
+    tokens = admitted = 0
+    for mode in wl.modes:
+        t0 = clock()
+        h = O.hash_chains_parallel(X.tokens, X.tok_offsets, X.principal, salts, mode,
+                                   X.boundary_tok, processes=processes)
+        t["chains"] += clock() - t0
+        tokens += 16 * h.shape[0]
+        t0 = clock()
+        O.Table().admit(h, bo)
+        t["admit"] += clock() - t0
+        admitted += X.n
+    dt = sum(t.values())
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": processes, "kind": "oracle",
+            "sample": (f"one full step of the same workload ({tokens} block tokens hashed, "
+                       f"{admitted} requests admitted, {len(wl.modes)} modes) in {dt:.1f} s; "
+                       f"chains over {processes} worker processes, salts and admission in one "
+                       "process"),
+            "seconds": dt, "requests_admitted_per_s": admitted / dt,
+            "phases": {
+                "salts_us_per_key": t["salts"] / wl.P * 1e6,
+                "chains_tokens_per_s": tokens / t["chains"],
+                "admit_requests_per_s": admitted / t["admit"],
+                "admit_rows_per_s": tokens / 16 / t["admit"],
             },
             "host": host_cpu_info()}
 
@@ -459,6 +524,11 @@ def main():
     main_s = torch.cuda.current_stream()
     streams = {m: torch.cuda.Stream(device=dev) for m in modes}  # default priority
     ev_chain, ev_look, ev_salts, ev_clear, ev_ins = [], [], [], [], []
+    # admission: one lookup-then-insert call over both batches, in order
+    admission = wl.name == "admission"
+    ev_adm = []
+    adm_hits = {m: torch.empty(X.n, dtype=torch.int32, device=dev) for m in modes}
+    adm_new = {m: torch.empty(X.n, dtype=torch.int32, device=dev) for m in modes}
 
     def bview(m):
         return out[m][0:nA], (out[m][0:nA] if relookup_same else out[m][nA:])
@@ -547,18 +617,26 @@ def main():
                 if record:
                     e1.record(s)
                     ev_chain.append((m, e0, e1))
-                end = timed(ev_ins, m, s) if record else None
-                caches[m].insert(hA, boA, sync=False, stream=s)
-                if end:
-                    end()
-            if record:
-                l0 = torch.cuda.Event(enable_timing=True)
-                l1 = torch.cuda.Event(enable_timing=True)
-                l0.record(s)
-            caches[m].lookup(hB, boB, out=hits[m], stream=s)
-            if record:
-                l1.record(s)
-                ev_look.append((m, l0, l1))
+                if admission:
+                    end = timed(ev_adm, m, s) if record else None
+                    caches[m].admit(out[m], x["blk_offsets"], sync=False, hits=adm_hits[m],
+                                    new=adm_new[m], stream=s)
+                    if end:
+                        end()
+                else:
+                    end = timed(ev_ins, m, s) if record else None
+                    caches[m].insert(hA, boA, sync=False, stream=s)
+                    if end:
+                        end()
+            if not admission:
+                if record:
+                    l0 = torch.cuda.Event(enable_timing=True)
+                    l1 = torch.cuda.Event(enable_timing=True)
+                    l0.record(s)
+                caches[m].lookup(hB, boB, out=hits[m], stream=s)
+                if record:
+                    l1.record(s)
+                    ev_look.append((m, l0, l1))
             ev = torch.cuda.Event()
             ev.record(s)
             done.append(ev)
@@ -585,6 +663,14 @@ def main():
     # a re-lookup of the inserted batch takes its expected hits from the
     # lookup batch the workload built for it
     exp = (wl.lookup if relookup_same else B).expect_hits
+    if admission:
+        # hits fixed by construction; each request's new blocks are the rest
+        # of its chain (chains share only a leading run of blocks)
+        exp = wl.notes["admit_hits"]
+        got_hits = {m: adm_hits[m].cpu().numpy() for m in modes}
+        got_new = {m: adm_new[m].cpu().numpy() for m in modes}
+        gates["G4_new_blocks_by_construction"] = all(
+            bool(np.array_equal(got_new[m], X.block_counts() - exp[m])) for m in modes)
     if exp is not None:
         gates["G4_hits_by_construction"] = all(
             bool(np.array_equal(got_hits[m], exp[m])) for m in modes)
@@ -630,8 +716,14 @@ def main():
             "table_slots": 1 << wl.log2_slots,
         },
     }
-    look_t = per(ev_look)
-    look_bytes = {m: lookup_bytes(cntB, got_hits[m]) for m in modes}
+    if admission:
+        # the admission call stands where the lookup stands in the other
+        # configs: its two kernels together, HBM-bound
+        look_t = per(ev_adm)
+        look_bytes = {m: admit_bytes(X.n, nX, n_keys[W.MODE_NAMES[m]]) for m in modes}
+    else:
+        look_t = per(ev_look)
+        look_bytes = {m: lookup_bytes(cntB, got_hits[m]) for m in modes}
     look_mean = {m: float(np.mean(ts)) for m, ts in look_t.items()}
     look_gbs = float(np.mean([look_bytes[m] / look_mean[m] for m in modes])) / 1e9
     g_look = 1  # lanes per request the library picks for this batch
@@ -651,6 +743,22 @@ def main():
             W.MODE_NAMES[m]: (look_bytes[m] - B.n * LOOKUP_BYTES_PER_REQUEST) //
             LOOKUP_BYTES_PER_BLOCK for m in modes},
     }
+    if admission:
+        atr = [recorded_traffic(k, wl.name, "cache")
+               for k in ("k_insert<true>", f"k_admit_scan<{admit_group(X.n, nX)}>")]
+        roof_lookup = {
+            "bound": "hbm", "kernel": "k_insert<true> + k_admit_scan (kvgov_cache_admit)",
+            "achieved": look_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": look_gbs / HBM_PEAK_GBS,
+            "traffic": None if None in atr else sum(t["bytes"] for t in atr),
+            "bytes_per_launch": {W.MODE_NAMES[m]: b for m, b in look_bytes.items()},
+            "launch_ms": {W.MODE_NAMES[m]: t * 1e3 for m, t in look_mean.items()},
+            "bytes_note": f"{INSERT_BYTES_NEW} B per new key, {INSERT_BYTES_PRESENT} B per "
+                          f"present key, {ADMIT_BYTES_PER_ROW} B per row (code write and "
+                          f"read, tag read), {ADMIT_BYTES_PER_REQUEST} B per request "
+                          "(offsets, two outputs); both kernels of the call",
+            "requests": X.n, "rows": nX,
+        }
     if probe_only:
         result["value"] = len(modes) * B.n / t_step
         result["unit"] = "lookups/s"
@@ -665,7 +773,10 @@ def main():
         result["value"] = 16 * blocks / t_step
         result["unit"] = "tokens/s"
         result["block_hashes_per_s"] = blocks / t_step
-        result["lookups_per_s"] = len(modes) * B.n / t_step
+        if admission:
+            result["requests_admitted_per_s"] = len(modes) * X.n / t_step
+        else:
+            result["lookups_per_s"] = len(modes) * B.n / t_step
         chain_t = per(ev_chain)
         ops = {m: OPS_PER_COMPRESSION * compressions(wl, X, m) for m in modes}
         mean_t = {m: float(np.mean(ts)) for m, ts in chain_t.items()}
@@ -711,7 +822,7 @@ def main():
             "concurrent_modes_achieved": concurrent,
             "concurrent_modes_frac": concurrent / INT_PEAK_TOPS,
         }
-        result["roofline_lookup"] = roof_lookup
+        result["roofline_admit" if admission else "roofline_lookup"] = roof_lookup
         per_step = [sum(chain_t[m][i] for m in modes) for i in range(args.steps)]
         if wl.name == "template":
             s = {W.MODE_NAMES[m]: int(got_hits[m].sum()) for m in modes}
@@ -740,6 +851,17 @@ def main():
                             "block_hashes_per_s": nX / sec,
                             "compressions_per_s": compressions(wl, X, m) / sec}
             ph["clear"] = stats(clear_t[m])
+        if admission:
+            st = stats(look_t[m])
+            sec = st["ms_median"] * 1e-3
+            b = look_bytes[m]
+            ph["admit"] = {**st, "requests": X.n, "rows": nX,
+                           "new_keys": n_keys[W.MODE_NAMES[m]],
+                           "requests_per_s": X.n / sec, "rows_per_s": nX / sec,
+                           "algorithmic_bytes": b, "gbs": b / sec / 1e9}
+            phases[W.MODE_NAMES[m]] = ph
+            continue
+        if not probe_only:
             st = stats(ins_t[m])
             sec = st["ms_median"] * 1e-3
             n_new = n_keys[W.MODE_NAMES[m]]
@@ -753,9 +875,9 @@ def main():
         phases[W.MODE_NAMES[m]] = ph
     result["phases"] = phases
 
-    if not probe_only:
+    if not probe_only and not admission:
         ins_gbs = float(np.mean([phases[W.MODE_NAMES[m]]["insert"]["gbs"] for m in modes]))
-        itr = recorded_traffic("k_insert", wl.name, "cache")
+        itr = recorded_traffic("k_insert<false>", wl.name, "cache")
         result["roofline_insert"] = {
             "bound": "hbm", "kernel": "k_insert (set-union insert)", "achieved": ins_gbs,
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ins_gbs / HBM_PEAK_GBS,
@@ -844,7 +966,7 @@ def main():
         roof = result["roofline"]
         if roof["bound"] == "alu":
             roof["frac_of_measured_peak"] = roof["achieved"] / mp["int_valu_tops"]
-        for key in ("roofline_lookup", "roofline_insert", "roofline"):
+        for key in ("roofline_lookup", "roofline_insert", "roofline_admit", "roofline"):
             rr = result.get(key)
             if rr and rr["bound"] == "hbm":
                 rr["frac_of_measured_gather32"] = rr["achieved"] / mp["gather32_gbs"]

@@ -350,6 +350,28 @@ def session(seed: int = SEED, n: int = 4096, P: int = 64) -> Workload:
                      "prefix_len": base.notes["prefix_len"]})
 
 
+def admission(seed: int = SEED, n: int = 4096, P: int = 64) -> Workload:
+    """The paper-shaped batches admitted in one call each mode: the insert
+    batch then the re-lookup batch, 2n requests in order.  Hits are fixed by
+    construction: a request sees the 132 prefix blocks once an earlier request
+    of its salting domain (root: the same principal; boundary: any request,
+    the prefix lies below the boundary) holds them, else nothing; the block
+    after the prefix mixes prefix and private tokens and is never shared.
+    notes["admit_hits"][mode] = int32 [2n]."""
+    base = paper(seed=seed, n=n, P=P)
+    pre = base.notes["prefix_len"] // BLOCK
+    prin = np.concatenate([base.insert.principal, base.lookup.principal])
+    first_of_principal = np.zeros(2 * n, dtype=bool)
+    first_of_principal[np.unique(prin, return_index=True)[1]] = True
+    root = np.where(first_of_principal, 0, pre).astype(np.int32)
+    bnd = np.full(2 * n, pre, dtype=np.int32)
+    bnd[0] = 0
+    notes = dict(base.notes)
+    notes["admit_hits"] = {ROOT: root, BOUNDARY: bnd}
+    return Workload("admission", base.K, base.principal_ids, base.insert, base.lookup,
+                    [ROOT, BOUNDARY], base.log2_slots, notes)
+
+
 CONFIGS = {
     "tiny": tiny,
     "paper": paper,
@@ -357,6 +379,7 @@ CONFIGS = {
     "probe": probe,
     "large": large,
     "session": session,
+    "admission": admission,
 }
 
 
