@@ -34,10 +34,10 @@
  *     waits for the stream.
  *   - K and the salts are secrets: the library keeps no copy of K after
  *     kvgov_salts returns and logs nothing.
- *   - The calls allocate no device memory except kvgov_cache_create and the
- *     stream-ordered scratch of kvgov_hash_chains and its resume variant,
- *     of kvgov_cache_admit (see there) and of the offset helpers (8 bytes
- *     per 1024 requests).
+ *   - The calls allocate no device memory except kvgov_cache_create,
+ *     kvgov_radix_create and the stream-ordered scratch of
+ *     kvgov_hash_chains and its resume variant, of kvgov_cache_admit (see
+ *     there) and of the offset helpers (8 bytes per 1024 requests).
  */
 #ifndef KVGOV_H
 #define KVGOV_H
@@ -265,6 +265,70 @@ int kvgov_cache_lookup(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
 int kvgov_cache_admit(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,
                       int32_t n, int64_t n_blocks, int32_t *hit_blocks, int32_t *new_blocks,
                       int64_t *n_new, void *stream);
+
+/*
+ * Radix index (Table tab:taxonomy, radix-tree prefix cache; Sec. 3.5: it
+ * reports the matched prefix length in tokens, finer than whole blocks;
+ * Sec. 4.1: sigma_p as the root node gives each principal a disjoint tree).
+ *
+ * A set of token sequences per tree: one tree per principal (KVGOV_ROOT,
+ * rooted at sigma_p) or one shared tree (KVGOV_NONE).  Boundary salting has
+ * no radix form in the paper: KVGOV_BOUNDARY returns KVGOV_E_UNSUPPORTED.
+ *   insert: adds every request's whole token sequence to its tree;
+ *   match:  match_len[r] = max over sequences s in r's tree of the number of
+ *           leading tokens r and s share (0 for an empty tree).
+ * Internally a trie of full-block nodes (the chained digests, as in the
+ * block cache) and token nodes for the first 1..15 tokens of each block
+ * below its parent: match = 16 * (block depth) + (tokens matched in the next
+ * block).
+ *
+ * create: block table of 2^log2_block_slots slots (~40 B each) and edge
+ * table of 2^log2_edge_slots slots (8 B each; up to 15 edges per distinct
+ * block, fewer where sequences share token prefixes), both in [4, 30], on the
+ * current device (which must be current for every later call:
+ * KVGOV_E_DEVICE otherwise).  Errors: KVGOV_E_INVAL, KVGOV_E_NOMEM,
+ * KVGOV_E_HIP.
+ */
+typedef struct kvgov_radix kvgov_radix;
+int kvgov_radix_create(int32_t log2_block_slots, int32_t log2_edge_slots, kvgov_radix **out);
+
+/* Frees the index (waits for the device first).  NULL is accepted. */
+int kvgov_radix_destroy(kvgov_radix *x);
+
+/* Empties both tables and the latched errors, in stream order. */
+int kvgov_radix_clear(kvgov_radix *x, void *stream);
+
+/*
+ * Inserts request r = 0..n-1: tokens[tok_offsets[r] .. tok_offsets[r+1]).
+ * tokens, n_tokens, tok_offsets, principal, salts, P, mode as for
+ * kvgov_hash_chains (mode NONE or ROOT).
+ * hashes, blk_offsets, n_blocks: the requests' chained block hashes as
+ *   kvgov_hash_chains computes them for the same tokens, mode and salts
+ *   (the index trusts them: other values give another index).
+ * Kernel errors (latched; kvgov_radix_stats returns them): KVGOV_E_OFFSETS
+ * (offsets out of range, or blk_offsets not matching len // 16; the request
+ * is skipped), KVGOV_E_PRINCIPAL, KVGOV_E_FULL (a table ran out of slots;
+ * clear before reuse).
+ */
+int kvgov_radix_insert(kvgov_radix *x, const int32_t *tokens, int64_t n_tokens,
+                       const int64_t *tok_offsets, int32_t n, const int32_t *principal,
+                       const uint8_t *salts, int32_t P, int32_t mode, const uint8_t *hashes,
+                       const int64_t *blk_offsets, int64_t n_blocks, void *stream);
+
+/*
+ * match_len (device out, int32 [n]) as defined above; arguments as for
+ * kvgov_radix_insert.  Reads the index only; sees every insert enqueued
+ * before it.  Kernel errors as for insert (a skipped request gets 0).
+ */
+int kvgov_radix_match(kvgov_radix *x, const int32_t *tokens, int64_t n_tokens,
+                      const int64_t *tok_offsets, int32_t n, const int32_t *principal,
+                      const uint8_t *salts, int32_t P, int32_t mode, const uint8_t *hashes,
+                      const int64_t *blk_offsets, int64_t n_blocks, int32_t *match_len,
+                      void *stream);
+
+/* Waits for `stream`; stores the number of block nodes (full-block digests
+ * and roots) and of edges (token nodes), and returns the latched error. */
+int kvgov_radix_stats(kvgov_radix *x, int64_t *block_nodes, int64_t *edges, void *stream);
 
 /* Waits for `stream`; stores the number of keys in T and returns the latched
  * error, if any. */

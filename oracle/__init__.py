@@ -15,7 +15,11 @@ What it computes, each piece plainly and in the paper's order:
                    digest h_{j0-1} (Sec. 2.1; Sec. 5.7, multi-turn sessions)
 * ``Table``        a set of block hashes; lookup returns the number of
                    leading blocks present, i.e. the first miss     (Sec. 2.1,
-                   Table "tab:taxonomy", block prefix cache row)
+                   Table "tab:taxonomy", block prefix cache row);
+                   admit = lookup-then-insert in request order
+* ``Radix``        token sequences per tree (per principal, or shared);
+                   match = longest shared token prefix (Table "tab:taxonomy",
+                   radix-tree row; Sec. 3.5; Sec. 4.1 per-principal root)
 
 SHA-256 and HMAC come from Python's ``hashlib``/``hmac`` (OpenSSL).  The
 package also carries its own FIPS 180-4 SHA-256 and RFC 2104 HMAC in plain
@@ -23,7 +27,9 @@ Python (``fips_sha256``, ``rfc2104``), used by the tests to pin the library
 routines; all pins are listed in the tests.
 """
 from .kvgov import (NONE, ROOT, BOUNDARY, BLOCK, salts, block_bytes, chain, chain_from,
-                    hash_chains, hash_chains_parallel, hash_chains_resume, Table, lookup_hits)
+                    hash_chains, hash_chains_parallel, hash_chains_resume, Table, lookup_hits,
+                    Radix, lcp_tokens)
 
 __all__ = ["NONE", "ROOT", "BOUNDARY", "BLOCK", "salts", "block_bytes", "chain", "chain_from",
-           "hash_chains", "hash_chains_parallel", "hash_chains_resume", "Table", "lookup_hits"]
+           "hash_chains", "hash_chains_parallel", "hash_chains_resume", "Table", "lookup_hits",
+           "Radix", "lcp_tokens"]

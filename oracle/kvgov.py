@@ -276,3 +276,55 @@ def lookup_hits(keys: set, hashes: np.ndarray, blk_offsets,
             j += 1
         out[i] = j
     return out
+
+
+# ---------------------------------------------------------------------------
+# radix-tree prefix cache (Table "tab:taxonomy", radix-tree row; Sec. 3.5;
+# Sec. 4.1: sigma_p as the root node gives each principal a disjoint tree)
+# ---------------------------------------------------------------------------
+
+def lcp_tokens(a: np.ndarray, b: np.ndarray) -> int:
+    """Number of leading tokens a and b share."""
+    n = min(len(a), len(b))
+    if n == 0:
+        return 0
+    diff = np.nonzero(np.asarray(a[:n]) != np.asarray(b[:n]))[0]
+    return int(diff[0]) if diff.size else n
+
+
+class Radix:
+    """Token sequences per tree: one tree per principal (root salting, keyed
+    by the principal's salt, the tree's root) or one shared tree (unsalted).
+    match(q) = max over the tree's sequences s of lcp_tokens(q, s)."""
+
+    def __init__(self):
+        self.trees = {}
+
+    @staticmethod
+    def _tree(mode: int, salt_bytes: Optional[bytes]):
+        if mode == NONE:
+            return b""
+        if mode == ROOT:
+            if salt_bytes is None or len(salt_bytes) != DIGEST:
+                raise ValueError("root salting needs a 32-byte salt")
+            return bytes(salt_bytes)
+        raise ValueError("the radix form exists for unsalted and root-salted trees only")
+
+    def insert(self, tokens, tok_offsets, principal, salt_list, mode) -> None:
+        tok_offsets = np.asarray(tok_offsets, dtype=np.int64)
+        for r in range(tok_offsets.shape[0] - 1):
+            s = salt_list[int(principal[r])] if mode != NONE else None
+            seq = np.array(tokens[int(tok_offsets[r]):int(tok_offsets[r + 1])], dtype=np.int64)
+            self.trees.setdefault(self._tree(mode, s), []).append(seq)
+
+    def match(self, tokens, tok_offsets, principal, salt_list, mode,
+              requests: Optional[Iterable[int]] = None) -> np.ndarray:
+        tok_offsets = np.asarray(tok_offsets, dtype=np.int64)
+        rows = range(tok_offsets.shape[0] - 1) if requests is None else list(requests)
+        out = []
+        for r in rows:
+            s = salt_list[int(principal[r])] if mode != NONE else None
+            q = np.array(tokens[int(tok_offsets[r]):int(tok_offsets[r + 1])], dtype=np.int64)
+            seqs = self.trees.get(self._tree(mode, s), [])
+            out.append(max([lcp_tokens(q, x) for x in seqs] or [0]))
+        return np.array(out, dtype=np.int32)

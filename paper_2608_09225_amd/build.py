@@ -10,7 +10,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIBS = {
-    "libkvgov.so": ["csrc/chains.hip", "csrc/cache.hip"],
+    "libkvgov.so": ["csrc/chains.hip", "csrc/cache.hip", "csrc/radix.hip"],
     "libkvgov_peaks.so": ["csrc/peaks.hip"],
 }
 OUT = os.path.join(HERE, "libkvgov.so")

@@ -43,66 +43,9 @@
 #include <atomic>
 #include <new>
 
-#include "common.h"
+#include "table.h"
 
 namespace kvgov {
-
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4), aligned(4)));
-
-// Counters are spread over kCounterLanes addresses (a workgroup adds to lane
-// blockIdx % kCounterLanes): atomics on one address serialise at ~10 ns each,
-// which at one atomic per wave dominated a 680k-key insert.  Readers sum.
-constexpr int kCounterLanes = 64;
-
-struct CacheMeta {
-  unsigned long long n_keys[kCounterLanes];       // keys in the table (all-0xFF key included)
-  unsigned long long new_keys[2][kCounterLanes];  // keys added by insert call `epoch`, at [epoch & 1]
-  unsigned long long exported;                    // keys written by the latest export
-  unsigned long long ones_tag;                    // the all-0xFF key's tag (0 = absent)
-  int32_t status;                                 // latched error (0 = none)
-  int32_t ones_present;                           // the all-0xFF key is in the table
-};
-
-struct TableView {
-  u32x4 *keys;  // 2 per slot
-  unsigned long long *tags;
-  CacheMeta *meta;
-  uint64_t mask;  // slots - 1
-};
-
-struct Key {
-  u32x4 lo, hi;
-};
-
-__device__ __forceinline__ Key load_key(const uint8_t *p) {
-  const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
-  return Key{q[0], q[1]};
-}
-
-__device__ __forceinline__ bool key_eq(const Key &a, const Key &b) {
-  const uint32_t d = (a.lo.x ^ b.lo.x) | (a.lo.y ^ b.lo.y) | (a.lo.z ^ b.lo.z) |
-                     (a.lo.w ^ b.lo.w) | (a.hi.x ^ b.hi.x) | (a.hi.y ^ b.hi.y) |
-                     (a.hi.z ^ b.hi.z) | (a.hi.w ^ b.hi.w);
-  return d == 0;
-}
-
-__device__ __forceinline__ bool key_is_empty_pattern(const Key &a) {
-  return (a.lo.x & a.lo.y & a.lo.z & a.lo.w & a.hi.x & a.hi.y & a.hi.z & a.hi.w) ==
-         0xFFFFFFFFu;
-}
-
-// Slot index from all 256 bits (keys are digests, but any 32-byte value is
-// valid, so every word takes part), finished with a 64-bit mixer.
-__device__ __forceinline__ uint64_t slot_hash(const Key &k) {
-  uint64_t x = ((uint64_t)k.lo.y << 32 | k.lo.x) ^
-               (((uint64_t)k.lo.w << 32 | k.lo.z) * 0x9E3779B97F4A7C15ull) ^
-               (((uint64_t)k.hi.y << 32 | k.hi.x) * 0xC2B2AE3D27D4EB4Full) ^
-               (((uint64_t)k.hi.w << 32 | k.hi.z) * 0x165667B19E3779F9ull);
-  x ^= x >> 31;
-  x *= 0xBF58476D1CE4E5B9ull;
-  x ^= x >> 29;
-  return x;
-}
 
 // ---------------------------------------------------------------------------
 // kernels
@@ -130,84 +73,6 @@ __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long l
     keys[2 * s + 1] = ones;
     tags[s] = 0;
   }
-}
-
-// Sum of v over the workgroup (256 threads), valid in thread 0.
-__device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t *lds4) {
-#pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) v += __shfl_xor(v, d, 64);
-  if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = v;
-  __syncthreads();
-  return threadIdx.x == 0 ? lds4[0] + lds4[1] + lds4[2] + lds4[3] : 0;
-}
-
-// Per-row codes written by the admission insert: the slot of the row's key,
-// or one of these (slots < 2^31, so no slot index collides with them).
-constexpr uint32_t kCodeOnes = 0xFFFFFFFEu;    // the all-0xFF key (tag in meta)
-constexpr uint32_t kCodeDup = 0xFFFFFFFDu;     // equals the previous request's key here
-constexpr uint32_t kCodeFailed = 0xFFFFFFFCu;  // not inserted (table full)
-
-// A tag claimed in this call (same epoch) whose row is above `mine`: lower
-// it.  Reads first, so most copies of a hot key issue no atomic.
-__device__ __forceinline__ void lower_claim(unsigned long long *tag, unsigned long long seen,
-                                            unsigned long long mine) {
-  if (mine < seen) atomicMin(tag, mine);
-}
-
-// Tags only ever change from 0 to a claim (and, within the claiming call, to
-// a smaller claim of the same key), so a plain (possibly stale) read can only
-// show 0 for a claimed slot; the compare-and-swap that follows then fails
-// and returns the claim.  Coherent atomics are used for the claim only.
-// Returns 1 if the key was added; *code receives where the key went.
-template <bool ADMIT>
-__device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &key, int64_t i,
-                                               int64_t lo, const uint8_t *hashes,
-                                               uint32_t epoch, uint32_t *code) {
-  const unsigned long long mine = ((unsigned long long)epoch << 32) |
-                                  (unsigned long long)(i - lo + 1);
-  if (key_is_empty_pattern(key)) {
-    *code = kCodeOnes;
-    unsigned long long expect = 0;
-    if (__hip_atomic_compare_exchange_strong(&t.meta->ones_tag, &expect, mine, __ATOMIC_RELAXED,
-                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-      atomicExch(&t.meta->ones_present, 1);
-      return 1;
-    }
-    if (ADMIT && (uint32_t)(expect >> 32) == epoch) lower_claim(&t.meta->ones_tag, expect, mine);
-    return 0;
-  }
-  uint64_t s = slot_hash(key) & t.mask;
-  for (uint64_t probes = 0; probes <= t.mask; ++probes) {
-    unsigned long long tag = t.tags[s];
-    if (tag == 0) {
-      unsigned long long expect = 0;
-      if (__hip_atomic_compare_exchange_strong(&t.tags[s], &expect, mine, __ATOMIC_RELAXED,
-                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-        t.keys[2 * s] = key.lo;
-        t.keys[2 * s + 1] = key.hi;
-        *code = (uint32_t)s;
-        return 1;
-      }
-      tag = expect;  // somebody claimed it first: examine the claimant
-    }
-    Key other;
-    const bool current = (uint32_t)(tag >> 32) == epoch;
-    if (current) {
-      const int64_t c = (int64_t)(tag & 0xFFFFFFFFull) - 1;
-      other = load_key(hashes + (lo + c) * 32);
-    } else {
-      other = Key{t.keys[2 * s], t.keys[2 * s + 1]};
-    }
-    if (key_eq(key, other)) {
-      if (ADMIT && current) lower_claim(&t.tags[s], tag, mine);
-      *code = (uint32_t)s;
-      return 0;
-    }
-    s = (s + 1) & t.mask;
-  }
-  atomicCAS(&t.meta->status, 0, KVGOV_E_FULL);
-  *code = kCodeFailed;
-  return 0;
 }
 
 // Consecutive keys per wave chunk of the insert.
@@ -303,19 +168,6 @@ __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hash
   }
 }
 
-// Is `key` in the table?  Reads the key array only.
-__device__ __forceinline__ bool probe(const TableView &t, const Key &key, bool ones_present) {
-  if (key_is_empty_pattern(key)) return ones_present;
-  uint64_t s = slot_hash(key) & t.mask;
-  for (uint64_t p = 0; p <= t.mask; ++p) {
-    const Key slot{t.keys[2 * s], t.keys[2 * s + 1]};
-    if (key_eq(slot, key)) return true;
-    if (key_is_empty_pattern(slot)) return false;
-    s = (s + 1) & t.mask;
-  }
-  return false;
-}
-
 struct LookupArgs {
   TableView t;
   const uint8_t *hashes;
@@ -336,7 +188,7 @@ __global__ __launch_bounds__(256) void k_lookup(LookupArgs a) {
   const int sub = (int)(gid % G);
   const int lane = threadIdx.x & 63;
   const int base = lane & ~(G - 1);
-  const uint64_t gmask = (G == 64) ? ~0ull : (((1ull << G) - 1ull) << base);
+  const uint64_t gmask = group_mask<G>(base);
   const int64_t b0 = a.blk_offsets[r], b1 = a.blk_offsets[r + 1];
   if (b0 < 0 || b1 < b0 || b1 > a.n_blocks) {
     if (sub == 0) {
@@ -416,7 +268,7 @@ __global__ __launch_bounds__(256) void k_admit_scan(AdmitArgs a) {
   const int sub = (int)(gid % G);
   const int lane = threadIdx.x & 63;
   const int base = lane & ~(G - 1);
-  const uint64_t gmask = (G == 64) ? ~0ull : (((1ull << G) - 1ull) << base);
+  const uint64_t gmask = group_mask<G>(base);
   const int64_t lo = a.blk_offsets[0], hi = a.blk_offsets[a.n];
   const int64_t b0 = a.blk_offsets[r], b1 = a.blk_offsets[r + 1];
   // the batch check of k_insert (which then wrote no codes), and this
@@ -509,14 +361,6 @@ __global__ __launch_bounds__(256) void k_export(TableView t, uint8_t *out, int64
 }  // namespace kvgov
 
 using namespace kvgov;
-
-struct kvgov_cache {
-  int device;
-  int32_t log2_slots;
-  int64_t slots;
-  TableView view;
-  std::atomic<uint32_t> epoch;
-};
 
 namespace {
 

@@ -14,6 +14,7 @@ Calls mirror the C ABI one to one:
     kvgov_hash_chains_resume -> hash_chains_resume(..., start_block, parents, ...)
     kvgov_resume_offsets -> resume_offsets(tok_offsets, start_block)
     kvgov_cache_*       -> Cache(log2_slots).insert / lookup / admit / clear / count / export
+    kvgov_radix_*       -> Radix(log2_block_slots, log2_edge_slots).insert / match / clear / stats
 """
 from __future__ import annotations
 
@@ -54,6 +55,15 @@ _SIGNATURES = {
     "kvgov_cache_lookup": (ctypes.c_int, [_vp, _vp, _vp, _c_i32, _c_i64, _vp, _vp]),
     "kvgov_cache_admit": (ctypes.c_int, [_vp, _vp, _vp, _c_i32, _c_i64, _vp, _vp,
                                          ctypes.POINTER(_c_i64), _vp]),
+    "kvgov_radix_create": (ctypes.c_int, [_c_i32, _c_i32, ctypes.POINTER(_vp)]),
+    "kvgov_radix_destroy": (ctypes.c_int, [_vp]),
+    "kvgov_radix_clear": (ctypes.c_int, [_vp, _vp]),
+    "kvgov_radix_insert": (ctypes.c_int, [_vp, _vp, _c_i64, _vp, _c_i32, _vp, _vp, _c_i32,
+                                          _c_i32, _vp, _vp, _c_i64, _vp]),
+    "kvgov_radix_match": (ctypes.c_int, [_vp, _vp, _c_i64, _vp, _c_i32, _vp, _vp, _c_i32,
+                                         _c_i32, _vp, _vp, _c_i64, _vp, _vp]),
+    "kvgov_radix_stats": (ctypes.c_int, [_vp, ctypes.POINTER(_c_i64), ctypes.POINTER(_c_i64),
+                                         _vp]),
     "kvgov_cache_count": (ctypes.c_int, [_vp, ctypes.POINTER(_c_i64), _vp]),
     "kvgov_cache_export": (ctypes.c_int, [_vp, _vp, _c_i64, ctypes.POINTER(_c_i64), _vp]),
 }
@@ -283,6 +293,7 @@ class Cache:
         h = _vp()
         _check(lib().kvgov_cache_create(int(log2_slots), ctypes.byref(h)), "kvgov_cache_create")
         self._h = h
+        self._pid = os.getpid()
         self.log2_slots = int(log2_slots)
 
     @property
@@ -363,9 +374,90 @@ class Cache:
         return buf[:int(v.value)]
 
     def close(self):
-        if self._h is not None:
+        # a forked child (e.g. a worker pool) inherits the object but not the
+        # GPU context: only the creating process frees the table
+        if self._h is not None and self._pid == os.getpid():
             _check(lib().kvgov_cache_destroy(self._h), "kvgov_cache_destroy")
-            self._h = None
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+# ---------------------------------------------------------------------------
+# radix index
+# ---------------------------------------------------------------------------
+
+class Radix:
+    """A kvgov_radix index on the current GPU (token-granular prefix match,
+    one tree per principal in root mode, one shared tree unsalted)."""
+
+    def __init__(self, log2_block_slots: int, log2_edge_slots: int):
+        h = _vp()
+        _check(lib().kvgov_radix_create(int(log2_block_slots), int(log2_edge_slots),
+                                        ctypes.byref(h)), "kvgov_radix_create")
+        self._h = h
+        self._pid = os.getpid()
+
+    @property
+    def handle(self):
+        if self._h is None or not self._h.value:
+            raise ValueError("radix index is closed")
+        return self._h
+
+    def clear(self, stream=None):
+        _check(lib().kvgov_radix_clear(self.handle, _stream(stream)), "kvgov_radix_clear")
+
+    def _args(self, tokens, tok_offsets, principal, salt_table, mode, hashes, blk_offsets):
+        tk = _dev(tokens, torch.int32, "tokens")
+        to = _dev(tok_offsets, torch.int64, "tok_offsets")
+        pr = _dev(principal, torch.int32, "principal", allow_none=(mode == NONE))
+        st = _dev(salt_table, torch.uint8, "salts", allow_none=(mode == NONE))
+        hs = _dev(hashes, torch.uint8, "hashes")
+        bo = _dev(blk_offsets, torch.int64, "blk_offsets")
+        P = 0 if st is None else int(st.shape[0])
+        return [_ptr(tk), tk.numel(), _ptr(to), to.numel() - 1, _ptr(pr), _ptr(st), P,
+                int(mode), _ptr(hs), _ptr(bo), hs.shape[0] if hs.dim() else 0]
+
+    def insert(self, tokens, tok_offsets, principal, salt_table, mode, hashes, blk_offsets,
+               stream=None):
+        """Adds each request's token sequence to its tree (asynchronous)."""
+        a = self._args(tokens, tok_offsets, principal, salt_table, mode, hashes, blk_offsets)
+        _check(lib().kvgov_radix_insert(self.handle, *a, _stream(stream)), "kvgov_radix_insert")
+
+    def match(self, tokens, tok_offsets, principal, salt_table, mode, hashes, blk_offsets,
+              out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+        """Matched prefix length in tokens per request (int32 [n])."""
+        a = self._args(tokens, tok_offsets, principal, salt_table, mode, hashes, blk_offsets)
+        if out is None:
+            out = torch.empty(a[3], dtype=torch.int32, device="cuda")
+        _dev(out, torch.int32, "out")
+        _check(lib().kvgov_radix_match(self.handle, *a, _ptr(out), _stream(stream)),
+               "kvgov_radix_match")
+        return out
+
+    def stats(self, stream=None):
+        """(block nodes, edges); waits and raises a latched error."""
+        b, e = _c_i64(), _c_i64()
+        _check(lib().kvgov_radix_stats(self.handle, ctypes.byref(b), ctypes.byref(e),
+                                       _stream(stream)), "kvgov_radix_stats")
+        return int(b.value), int(e.value)
+
+    def close(self):
+        # only the creating process frees the index (see Cache.close)
+        if getattr(self, "_h", None) is not None and self._h.value and \
+                self._pid == os.getpid():
+            _check(lib().kvgov_radix_destroy(self._h), "kvgov_radix_destroy")
+        self._h = None
 
     def __del__(self):
         try:

@@ -118,6 +118,17 @@ def test_host_validation_returns_before_any_launch():
     assert L.kvgov_cache_insert(None, fake, fake, 1, 4, None, None) == INVAL
     assert L.kvgov_cache_lookup(None, fake, fake, 1, 4, fake, None) == INVAL
     assert L.kvgov_cache_admit(None, fake, fake, 1, 4, fake, fake, None, None) == INVAL
+    # radix
+    assert L.kvgov_radix_create(3, 10, ctypes.byref(h)) == INVAL
+    assert L.kvgov_radix_create(10, 31, ctypes.byref(h)) == INVAL
+    assert L.kvgov_radix_create(10, 10, None) == INVAL
+    assert L.kvgov_radix_insert(None, fake, 64, fake, 2, fake, fake, 4, K.ROOT, fake, fake,
+                                4, None) == INVAL
+    assert L.kvgov_radix_match(None, fake, 64, fake, 2, fake, fake, 4, K.ROOT, fake, fake,
+                               4, fake, None) == INVAL
+    assert L.kvgov_radix_clear(None, None) == INVAL
+    assert L.kvgov_radix_stats(None, ctypes.byref(n), ctypes.byref(n), None) == INVAL
+    assert L.kvgov_radix_destroy(None) == 0
     assert L.kvgov_cache_clear(None, None) == INVAL
     assert L.kvgov_cache_count(None, ctypes.byref(n), None) == INVAL
     assert L.kvgov_cache_export(None, fake, 1, ctypes.byref(n), None) == INVAL
