@@ -78,6 +78,16 @@ LOOKUP_BYTES_PER_REQUEST = 20
 # a key already present reads the query and the slot holding it.
 INSERT_BYTES_NEW = 96
 INSERT_BYTES_PRESENT = 64
+# Radix match: the block lookup's bytes, plus per request the 32-byte key of
+# the last matched block (its node) and per token step one 8-byte edge key
+# and the 4-byte token.  Radix insert: per record (full or partial block) its
+# parent key (32 B) and per edge the 4-byte token and the 8-byte edge slot
+# (read, and written when new).
+RADIX_MATCH_BYTES_NODE = 32
+RADIX_MATCH_BYTES_STEP = 12
+RADIX_INSERT_BYTES_RECORD = 32
+RADIX_INSERT_BYTES_EDGE = 12
+RADIX_EDGE_SLOTS_LOG2 = 23
 # Admission: the insert's bytes, plus per row a 4-byte code written and read
 # back and an 8-byte tag read; per request two 8-byte offsets and two 4-byte
 # outputs.
@@ -95,6 +105,9 @@ DESCRIPTIONS = {
              "1M probes of U{{8..64}} blocks, 70% own-principal prefixes, 30% foreign",
     "large": "large batch: 65536 requests, lognormal lengths (median 2048, sigma 1, max "
              "32768 tokens), 4096 principals, root and boundary; chains + insert + re-lookup",
+    "radix": "paper-shaped batches on the radix index: 4096 insert-batch sequences inserted, "
+             "4096 re-lookup-batch requests matched token by token, 64 principals, root "
+             "(per-principal trees) and unsalted; chains + clear + insert + match",
     "admission": "paper-shaped batches admitted in order: 8192 requests (4096 insert-batch "
                  "then 4096 re-lookup-batch), 64 principals, root and boundary (token 2119); "
                  "chains + one lookup-then-insert call per mode",
@@ -111,7 +124,8 @@ def log(*a):
 # Kernel sources whose hash identifies the build a traffic record was taken on.
 KERNEL_SOURCES = {
     "chains": ["chains.hip", "sha256_cdna4.h", "common.h"],
-    "cache": ["cache.hip", "common.h"],
+    "cache": ["cache.hip", "table.h", "common.h"],
+    "radix": ["radix.hip", "table.h", "common.h"],
 }
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "hbm_traffic.md")
 
@@ -167,6 +181,23 @@ def compressions(wl: W.Workload, batch: W.Batch, mode: int) -> int:
         k = batch.boundary_tok.astype(np.int64) // W.BLOCK
         c += int(((k > 0) & (k < nf) & (k >= j0)).sum())
     return c
+
+
+def radix_match_bytes(counts: np.ndarray, match: np.ndarray) -> int:
+    """Algorithmic bytes of one radix match launch: the block lookup up to
+    the first absent block, the node key of the last matched block, and the
+    edge steps (the matched ones and the failing one)."""
+    hits = np.minimum(match.astype(np.int64) // 16, counts)
+    return (lookup_bytes(counts, hits) + RADIX_MATCH_BYTES_NODE * counts.size +
+            RADIX_MATCH_BYTES_STEP * int((match.astype(np.int64) % 16 + 1).sum()))
+
+
+def radix_insert_edges(batch: W.Batch) -> int:
+    """Edges the insert walks: the first min(len, 15) tokens of every full or
+    partial block."""
+    L = batch.lengths.astype(np.int64)
+    tail = L % 16
+    return int(15 * (L // 16).sum() + tail.sum())
 
 
 def admit_bytes(n_req: int, rows: int, n_new: int) -> int:
@@ -241,6 +272,8 @@ def cpu_baseline(wl: W.Workload, processes: int, max_blocks: int):
         return cpu_baseline_session(wl, processes)
     if wl.name == "admission":
         return cpu_baseline_admission(wl, processes)
+    if wl.name == "radix":
+        return cpu_baseline_radix(wl, processes)
     same = wl.name == "large"
     A = capped(wl.insert, max_blocks)
     B = A if same else capped(wl.lookup, max_blocks)
@@ -296,6 +329,51 @@ def cpu_baseline(wl: W.Workload, processes: int, max_blocks: int):
                 "sample": f"chains of the first {one.n} insert requests, "
                           f"{W.MODE_NAMES[wl.modes[0]]} mode",
                 "salts_us_per_key": cpu_salt_cost(wl) * 1e6,
+            },
+            "host": host_cpu_info()}
+
+
+def cpu_baseline_radix(wl: W.Workload, processes: int, sample: int = 128):
+    """The oracle's chains of both batches (over worker processes), its radix
+    insert of the insert batch and its match of the first ``sample`` requests
+    of the re-lookup batch (one process; the match time is scaled to the
+    whole batch, stated in ``sample``)."""
+    import oracle as O
+    A, B = wl.insert, wl.lookup
+    X = concat(A, B)
+    clock = time.perf_counter
+    t = {"salts": 0.0, "chains": 0.0, "insert": 0.0, "match": 0.0}
+    t0 = clock()
+    salts = O.salts(wl.K, wl.principal_ids)
+    t["salts"] = clock() - t0
+    tokens = 0
+    q = np.arange(min(sample, B.n))
+    for mode in wl.modes:
+        t0 = clock()
+        h = O.hash_chains_parallel(X.tokens, X.tok_offsets, X.principal, salts, mode,
+                                   X.boundary_tok, processes=processes)
+        t["chains"] += clock() - t0
+        tokens += 16 * h.shape[0]
+        R = O.Radix()
+        t0 = clock()
+        R.insert(A.tokens, A.tok_offsets, A.principal, salts, mode)
+        t["insert"] += clock() - t0
+        t0 = clock()
+        R.match(B.tokens, B.tok_offsets, B.principal, salts, mode, requests=q)
+        t["match"] += (clock() - t0) * B.n / q.size
+    dt = sum(t.values())
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": processes, "kind": "oracle",
+            "sample": (f"chains of both batches ({tokens} block tokens) and the radix insert "
+                       f"of the insert batch in full, the match of {q.size} of the {B.n} "
+                       f"re-lookup requests scaled to the batch ({len(wl.modes)} modes); "
+                       f"{dt:.1f} s with the scaling; chains over {processes} worker "
+                       "processes, the rest in one process"),
+            "seconds": dt, "matches_per_s": len(wl.modes) * B.n / dt,
+            "phases": {
+                "salts_us_per_key": t["salts"] / wl.P * 1e6,
+                "chains_tokens_per_s": tokens / t["chains"],
+                "radix_insert_sequences_per_s": len(wl.modes) * A.n / t["insert"],
+                "radix_match_per_s": len(wl.modes) * B.n / t["match"],
             },
             "host": host_cpu_info()}
 
@@ -520,7 +598,12 @@ def main():
     hits = {m: torch.empty(B.n, dtype=torch.int32, device=dev) for m in modes}
     salts = torch.empty((wl.P, 32), dtype=torch.uint8, device=dev)
     status = K.new_status(dev)
-    caches = {m: K.Cache(wl.log2_slots) for m in modes}
+    radix_cfg = wl.name == "radix"
+    caches = {m: K.Cache(wl.log2_slots) for m in modes} if not radix_cfg else {}
+    radixes = {m: K.Radix(wl.log2_slots, RADIX_EDGE_SLOTS_LOG2) for m in modes} \
+        if radix_cfg else {}
+    matched = {m: torch.empty(B.n, dtype=torch.int32, device=dev) for m in modes}
+    ev_rins, ev_rmatch = [], []
     main_s = torch.cuda.current_stream()
     streams = {m: torch.cuda.Stream(device=dev) for m in modes}  # default priority
     ev_chain, ev_look, ev_salts, ev_clear, ev_ins = [], [], [], [], []
@@ -604,7 +687,7 @@ def main():
             if not probe_only:
                 # the table clear needs no salts: it overlaps the salts kernel
                 end = timed(ev_clear, m, s) if record else None
-                caches[m].clear(stream=s)
+                (radixes if radix_cfg else caches)[m].clear(stream=s)
                 if end:
                     end()
             s.wait_event(salted)
@@ -617,7 +700,24 @@ def main():
                 if record:
                     e1.record(s)
                     ev_chain.append((m, e0, e1))
-                if admission:
+                if radix_cfg:
+                    # insert batch A's sequences, match batch B's (views of
+                    # the concatenated arrays: A's requests come first)
+                    pr = x["principal"] if m != W.NONE else None
+                    sd = salts if m != W.NONE else None
+                    end = timed(ev_rins, m, s) if record else None
+                    radixes[m].insert(x["tokens"], x["tok_offsets"][:A.n + 1],
+                                      None if pr is None else pr[:A.n], sd, m, out[m],
+                                      x["blk_offsets"][:A.n + 1], stream=s)
+                    if end:
+                        end()
+                    end = timed(ev_rmatch, m, s) if record else None
+                    radixes[m].match(x["tokens"], x["tok_offsets"][A.n:],
+                                     None if pr is None else pr[A.n:], sd, m, out[m],
+                                     x["blk_offsets"][A.n:], out=matched[m], stream=s)
+                    if end:
+                        end()
+                elif admission:
                     end = timed(ev_adm, m, s) if record else None
                     caches[m].admit(out[m], x["blk_offsets"], sync=False, hits=adm_hits[m],
                                     new=adm_new[m], stream=s)
@@ -628,7 +728,7 @@ def main():
                     caches[m].insert(hA, boA, sync=False, stream=s)
                     if end:
                         end()
-            if not admission:
+            if not admission and not radix_cfg:
                 if record:
                     l0 = torch.cuda.Event(enable_timing=True)
                     l1 = torch.cuda.Event(enable_timing=True)
@@ -657,7 +757,11 @@ def main():
 
     # ---- gates: latched errors, bit-exactness on a sample, by-construction hits
     K.check_status(status, "bench step")
-    n_keys = {W.MODE_NAMES[m]: caches[m].count() for m in modes}
+    if radix_cfg:
+        rstats = {W.MODE_NAMES[m]: radixes[m].stats() for m in modes}
+        n_keys = {k: v[0] for k, v in rstats.items()}
+    else:
+        n_keys = {W.MODE_NAMES[m]: caches[m].count() for m in modes}
     gates = {}
     got_hits = {m: hits[m].cpu().numpy() for m in modes}
     # a re-lookup of the inserted batch takes its expected hits from the
@@ -671,6 +775,13 @@ def main():
         got_new = {m: adm_new[m].cpu().numpy() for m in modes}
         gates["G4_new_blocks_by_construction"] = all(
             bool(np.array_equal(got_new[m], X.block_counts() - exp[m])) for m in modes)
+    if radix_cfg:
+        exp = None
+        got_match = {m: matched[m].cpu().numpy() for m in modes}
+        # every request of the matched batch shares the 2119-token prefix with
+        # inserted requests of its principal (root) or of any principal
+        gates["G4_match_covers_shared_prefix"] = all(
+            bool((got_match[m] >= wl.notes["prefix_len"]).all()) for m in modes)
     if exp is not None:
         gates["G4_hits_by_construction"] = all(
             bool(np.array_equal(got_hits[m], exp[m])) for m in modes)
@@ -689,6 +800,14 @@ def main():
             want = O.hash_chains(X.tokens, X.tok_offsets, X.principal, osalts, m,
                                  X.boundary_tok, requests=[int(r)])[j0X[r]:]
             ok &= bool(np.array_equal(got[bo[r]:bo[r + 1]], want))
+    if radix_cfg:
+        # sampled match lengths against the oracle's index of the insert batch
+        qs = np.sort(gs.choice(B.n, min(96, B.n), replace=False))
+        for m in modes:
+            R = O.Radix()
+            R.insert(A.tokens, A.tok_offsets, A.principal, osalts, m)
+            want = R.match(B.tokens, B.tok_offsets, B.principal, osalts, m, requests=qs)
+            ok &= bool(np.array_equal(got_match[m][qs], want))
     gates["G1_bitexact_sampled"] = bool(ok)
 
     def per(evs):
@@ -721,6 +840,9 @@ def main():
         # configs: its two kernels together, HBM-bound
         look_t = per(ev_adm)
         look_bytes = {m: admit_bytes(X.n, nX, n_keys[W.MODE_NAMES[m]]) for m in modes}
+    elif radix_cfg:
+        look_t = per(ev_rmatch)
+        look_bytes = {m: radix_match_bytes(B.block_counts(), got_match[m]) for m in modes}
     else:
         look_t = per(ev_look)
         look_bytes = {m: lookup_bytes(cntB, got_hits[m]) for m in modes}
@@ -759,6 +881,22 @@ def main():
                           "(offsets, two outputs); both kernels of the call",
             "requests": X.n, "rows": nX,
         }
+    if radix_cfg:
+        g_r = 64 if admit_group(B.n, int(B.block_counts().sum())) > 16 else 16
+        rtr = recorded_traffic(f"k_radix_match<{g_r}>", wl.name, "radix")
+        roof_lookup = {
+            "bound": "hbm", "kernel": f"k_radix_match<{g_r}> (token-granular match)",
+            "achieved": look_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": look_gbs / HBM_PEAK_GBS, "traffic": None if rtr is None else rtr["bytes"],
+            "bytes_per_launch": {W.MODE_NAMES[m]: b for m, b in look_bytes.items()},
+            "launch_ms": {W.MODE_NAMES[m]: t * 1e3 for m, t in look_mean.items()},
+            "bytes_note": f"block lookup up to the first absent block "
+                          f"({LOOKUP_BYTES_PER_BLOCK} B per examined block, "
+                          f"{LOOKUP_BYTES_PER_REQUEST} B per request), "
+                          f"{RADIX_MATCH_BYTES_NODE} B node key per request, "
+                          f"{RADIX_MATCH_BYTES_STEP} B per edge step",
+            "mean_match_tokens": {W.MODE_NAMES[m]: float(got_match[m].mean()) for m in modes},
+        }
     if probe_only:
         result["value"] = len(modes) * B.n / t_step
         result["unit"] = "lookups/s"
@@ -775,6 +913,8 @@ def main():
         result["block_hashes_per_s"] = blocks / t_step
         if admission:
             result["requests_admitted_per_s"] = len(modes) * X.n / t_step
+        elif radix_cfg:
+            result["matches_per_s"] = len(modes) * B.n / t_step
         else:
             result["lookups_per_s"] = len(modes) * B.n / t_step
         chain_t = per(ev_chain)
@@ -822,7 +962,8 @@ def main():
             "concurrent_modes_achieved": concurrent,
             "concurrent_modes_frac": concurrent / INT_PEAK_TOPS,
         }
-        result["roofline_admit" if admission else "roofline_lookup"] = roof_lookup
+        result["roofline_admit" if admission else
+               "roofline_radix_match" if radix_cfg else "roofline_lookup"] = roof_lookup
         per_step = [sum(chain_t[m][i] for m in modes) for i in range(args.steps)]
         if wl.name == "template":
             s = {W.MODE_NAMES[m]: int(got_hits[m].sum()) for m in modes}
@@ -861,6 +1002,25 @@ def main():
                            "algorithmic_bytes": b, "gbs": b / sec / 1e9}
             phases[W.MODE_NAMES[m]] = ph
             continue
+        if radix_cfg:
+            nb, ne = rstats[W.MODE_NAMES[m]]
+            st = stats(per(ev_rins)[m])
+            sec = st["ms_median"] * 1e-3
+            edges = radix_insert_edges(A)
+            recs = int(((A.lengths + 15) // 16).sum())
+            b = (INSERT_BYTES_NEW * nb + INSERT_BYTES_PRESENT * max(nA - nb, 0) +
+                 RADIX_INSERT_BYTES_RECORD * recs + RADIX_INSERT_BYTES_EDGE * edges)
+            ph["radix_insert"] = {**st, "sequences": A.n, "tokens": int(A.lengths.sum()),
+                                  "block_nodes": nb, "edges_walked": edges,
+                                  "edges_in_index": ne, "sequences_per_s": A.n / sec,
+                                  "algorithmic_bytes": b, "gbs": b / sec / 1e9}
+            st = stats(look_t[m])
+            sec = st["ms_median"] * 1e-3
+            ph["radix_match"] = {**st, "matches_per_s": B.n / sec,
+                                 "algorithmic_bytes": look_bytes[m],
+                                 "gbs": look_bytes[m] / sec / 1e9}
+            phases[W.MODE_NAMES[m]] = ph
+            continue
         if not probe_only:
             st = stats(ins_t[m])
             sec = st["ms_median"] * 1e-3
@@ -875,7 +1035,24 @@ def main():
         phases[W.MODE_NAMES[m]] = ph
     result["phases"] = phases
 
-    if not probe_only and not admission:
+    if radix_cfg:
+        ins_gbs = float(np.mean([phases[W.MODE_NAMES[m]]["radix_insert"]["gbs"]
+                                 for m in modes]))
+        g_i = admit_group(A.n, nA)
+        itr = [recorded_traffic(k, wl.name, t) for k, t in
+               (("k_radix_roots", "radix"), ("k_insert<false>", "cache"),
+                (f"k_radix_edges<{g_i}>", "radix"))]
+        result["roofline_radix_insert"] = {
+            "bound": "hbm", "kernel": f"k_radix_roots + k_insert + k_radix_edges<{g_i}> "
+                                      "(kvgov_radix_insert)",
+            "achieved": ins_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": ins_gbs / HBM_PEAK_GBS,
+            "traffic": None if None in itr else sum(t["bytes"] for t in itr),
+            "bytes_note": f"the block insert's {INSERT_BYTES_NEW}/{INSERT_BYTES_PRESENT} B per "
+                          f"new/present key, {RADIX_INSERT_BYTES_RECORD} B per record (parent "
+                          f"key), {RADIX_INSERT_BYTES_EDGE} B per edge walked",
+        }
+    if not probe_only and not admission and not radix_cfg:
         ins_gbs = float(np.mean([phases[W.MODE_NAMES[m]]["insert"]["gbs"] for m in modes]))
         itr = recorded_traffic("k_insert<false>", wl.name, "cache")
         result["roofline_insert"] = {
@@ -966,7 +1143,8 @@ def main():
         roof = result["roofline"]
         if roof["bound"] == "alu":
             roof["frac_of_measured_peak"] = roof["achieved"] / mp["int_valu_tops"]
-        for key in ("roofline_lookup", "roofline_insert", "roofline_admit", "roofline"):
+        for key in ("roofline_lookup", "roofline_insert", "roofline_admit",
+                    "roofline_radix_match", "roofline_radix_insert", "roofline"):
             rr = result.get(key)
             if rr and rr["bound"] == "hbm":
                 rr["frac_of_measured_gather32"] = rr["achieved"] / mp["gather32_gbs"]
@@ -980,7 +1158,7 @@ def main():
         procs = min(16, len(os.sched_getaffinity(0)))
         log(f"timing the CPU oracle on {procs} processes")
         result["cpu_baseline"] = cpu_baseline(wl, procs, max_blocks=1_500_000)
-    for c in caches.values():
+    for c in list(caches.values()) + list(radixes.values()):
         c.close()
     print(json.dumps(result), flush=True)
     if not (gates["G1_bitexact_sampled"] and gates.get("G4_hits_by_construction", True)):

@@ -410,6 +410,15 @@ int read_new_keys(kvgov_cache *c, uint32_t epoch, int64_t *n_new, hipStream_t s)
 
 }  // namespace
 
+int kvgov::cache_insert_rows(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,
+                             int32_t n, int64_t n_blocks, hipStream_t s, uint32_t *epoch) {
+  *epoch = c->epoch.fetch_add(1) + 1;
+  if (*epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;  // 2^32 - 1 inserts since clear
+  hipLaunchKernelGGL(k_insert<false>, dim3(insert_grid(n_blocks)), dim3(256), 0, s, c->view,
+                     hashes, blk_offsets, n, n_blocks, *epoch, nullptr);
+  return launch_status();
+}
+
 extern "C" {
 
 int kvgov_cache_create(int32_t log2_slots, kvgov_cache **out) {
@@ -480,11 +489,8 @@ int kvgov_cache_insert(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
   int rc = check_device(c);
   if (rc != KVGOV_OK) return rc;
   hipStream_t s = as_stream(stream);
-  uint32_t epoch = c->epoch.fetch_add(1) + 1;
-  if (epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;  // 2^32 - 1 inserts since clear
-  hipLaunchKernelGGL(k_insert<false>, dim3(insert_grid(n_blocks)), dim3(256), 0, s, c->view,
-                     hashes, blk_offsets, n, n_blocks, epoch, nullptr);
-  rc = launch_status();
+  uint32_t epoch = 0;
+  rc = cache_insert_rows(c, hashes, blk_offsets, n, n_blocks, s, &epoch);
   if (rc != KVGOV_OK || !n_new) return rc;
   return read_new_keys(c, epoch, n_new, s);
 }

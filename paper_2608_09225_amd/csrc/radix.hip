@@ -139,6 +139,7 @@ struct RadixArgs {
   const int64_t *blk_offsets;
   int64_t n_blocks;
   int32_t *match_len;  // match only
+  uint32_t blk_epoch;  // insert only: the epoch of the call's block insert
 };
 
 // Request r's token range, full-block rows and root key, or false (latched).
@@ -173,7 +174,13 @@ __device__ __forceinline__ bool radix_req(const RadixArgs &a, int64_t r, RadixRe
 }
 
 // Insert: G lanes per request, one (possibly partial) block each: the edges
-// of its first min(len, 15) tokens below its parent block node.
+// of its first min(len, 15) tokens below its parent block node.  The edges
+// of a full block j are fixed by h_j (its parent and its tokens), so only
+// the row that claimed h_j in this call's block insert walks them: a block
+// present before the call has them already, and every other row holding
+// h_j would repeat them (thousands of rows of a shared prefix would
+// otherwise contend on the same edge slots).  A partial last block has no
+// digest and always walks its edges.
 template <int G>
 __global__ __launch_bounds__(256) void k_radix_edges(RadixArgs a) {
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -184,7 +191,20 @@ __global__ __launch_bounds__(256) void k_radix_edges(RadixArgs a) {
   if (!radix_req(a, r, q)) return;
   uint32_t added = 0;
   const int64_t nrec = (q.len + 15) >> 4;  // full blocks and a partial tail
+  const int64_t lo = a.blk_offsets[0];
   for (int64_t j = sub; j < nrec; j += G) {
+    if (j < q.nf) {
+      const int64_t f = q.b0 + j;
+      const int64_t slot = find_slot(a.t, load_key(a.hashes + f * 32));
+      if (slot >= 0) {
+        const unsigned long long tag = a.t.tags[slot];
+        if ((uint32_t)(tag >> 32) != a.blk_epoch ||
+            (int64_t)(tag & 0xFFFFFFFFull) - 1 != f - lo)
+          continue;  // not this row's block to expand
+      }
+      // slot < 0: the all-0xFF digest (no tag: expand, edges are idempotent)
+      // or a block the full table could not take (the walk below latches)
+    }
     uint32_t node = block_node(a.t, load_key(j == 0 ? q.root : a.hashes + (q.b0 + j - 1) * 32));
     if (node == kNoNode) {
       // the parent block was not inserted (a full table, latched there)
@@ -402,7 +422,7 @@ int kvgov_radix_insert(kvgov_radix *x, const int32_t *tokens, int64_t n_tokens,
                      c->view, roots, n_roots, epoch);
   rc = launch_status();
   if (rc != KVGOV_OK) return rc;
-  rc = kvgov_cache_insert(c, hashes, blk_offsets, n, n_blocks, nullptr, stream);
+  rc = cache_insert_rows(c, hashes, blk_offsets, n, n_blocks, s, &a.blk_epoch);
   if (rc != KVGOV_OK) return rc;
   const int g = radix_group(n, n_blocks);
   const dim3 grid((unsigned)ceil_div((int64_t)n * g, 256)), block(256);

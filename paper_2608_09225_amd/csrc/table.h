@@ -180,6 +180,12 @@ __device__ __forceinline__ int64_t find_slot(const TableView &t, const Key &key)
   return -1;
 }
 
+// Enqueues the plain set-union insert of a batch's rows (cache.hip); stores
+// the call's epoch, whose tags mark the slots the call claimed, each with
+// the row that claimed it.
+int cache_insert_rows(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,
+                      int32_t n, int64_t n_blocks, hipStream_t s, uint32_t *epoch);
+
 }  // namespace kvgov
 
 // The table object behind kvgov_cache *.

@@ -372,6 +372,17 @@ def admission(seed: int = SEED, n: int = 4096, P: int = 64) -> Workload:
                     [ROOT, BOUNDARY], base.log2_slots, notes)
 
 
+def radix(seed: int = SEED, n: int = 4096, P: int = 64) -> Workload:
+    """The paper-shaped batches on the radix index: the insert batch's token
+    sequences go into the index, the re-lookup batch is matched (token
+    granular: every match is at least the 2119-token shared prefix, more
+    where a fresh suffix happens to continue an inserted one).  Root salting
+    (one tree per principal) and unsalted (one tree)."""
+    base = paper(seed=seed, n=n, P=P)
+    return Workload("radix", base.K, base.principal_ids, base.insert, base.lookup,
+                    [ROOT, NONE], base.log2_slots, dict(base.notes))
+
+
 CONFIGS = {
     "tiny": tiny,
     "paper": paper,
@@ -380,6 +391,7 @@ CONFIGS = {
     "large": large,
     "session": session,
     "admission": admission,
+    "radix": radix,
 }
 
 
