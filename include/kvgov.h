@@ -36,8 +36,9 @@
  *     kvgov_salts returns and logs nothing.
  *   - The calls allocate no device memory except kvgov_cache_create,
  *     kvgov_radix_create and the stream-ordered scratch of
- *     kvgov_hash_chains and its resume variant, of kvgov_cache_admit (see
- *     there) and of the offset helpers (8 bytes per 1024 requests).
+ *     kvgov_hash_chains and its resume variant, of kvgov_cache_admit, of
+ *     the maintenance calls (see there) and of the offset helpers (8 bytes
+ *     per 1024 requests).
  */
 #ifndef KVGOV_H
 #define KVGOV_H
@@ -265,6 +266,45 @@ int kvgov_cache_lookup(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
 int kvgov_cache_admit(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,
                       int32_t n, int64_t n_blocks, int32_t *hit_blocks, int32_t *new_blocks,
                       int64_t *n_new, void *stream);
+
+/*
+ * Table maintenance (the paper gives none; a serving cache needs it).
+ *
+ * Recency, on a table that tracks it (kvgov_cache_set_recency; off after
+ * create): every kvgov_cache_insert or kvgov_cache_admit call is one tick of
+ * the table's clock (its call number since the last clear); each key of its
+ * batch takes the tick as its stamp and the smallest row position (within
+ * its request) it has in that batch as its depth.  Lookups do not change
+ * recency.  Keys inserted while tracking is off rank below every tracked
+ * key.  Tracking costs each insert and admission a read of the key's
+ * recency word and, where it grows, an atomic.
+ *
+ * evict: keeps the largest set of whole (stamp, depth) classes, newest stamp
+ * first and, within a stamp, shallowest depth first, that holds at most
+ * max_keys keys, and removes the rest (KVGOV_E_UNSUPPORTED on a table that
+ * does not track recency).  When every insert and admission passes whole
+ * chains from block 0 (as kvgov_hash_chains lays them out), a chain's
+ * earlier block never ranks below a later one, so the kept keys of every
+ * chain form a prefix of it.  (Batches holding only a chain's suffix, such
+ * as resumed chains, can leave suffix blocks ranked above their prefix;
+ * lookups stay correct, stopping at the first absent block, and the
+ * unreachable blocks go at a later eviction.)
+ * erase: removes exactly the given keys (device, uint8 [n_keys][32]; keys not
+ * in T are ignored), tracking or not.
+ *
+ * Both rebuild the table from the keys they keep (no tombstones: lookups
+ * keep reading one key per probe), in stream order.  n_kept / n_erased: host
+ * out or NULL; non-NULL waits for `stream`, stores the keys kept / the
+ * distinct present keys erased, and returns any latched error.
+ * Scratch: 40 * (slots + 1) bytes + 2 KiB from hipMallocAsync on `stream`,
+ * freed in stream order.  Errors: KVGOV_E_INVAL, KVGOV_E_NOMEM,
+ * KVGOV_E_UNSUPPORTED (as above, or 2^32 - 1 calls since the last clear),
+ * KVGOV_E_HIP, KVGOV_E_DEVICE.
+ */
+int kvgov_cache_set_recency(kvgov_cache *c, int32_t on);
+int kvgov_cache_evict(kvgov_cache *c, int64_t max_keys, int64_t *n_kept, void *stream);
+int kvgov_cache_erase(kvgov_cache *c, const uint8_t *keys, int64_t n_keys, int64_t *n_erased,
+                      void *stream);
 
 /*
  * Radix index (Table tab:taxonomy, radix-tree prefix cache; Sec. 3.5: it

@@ -221,22 +221,84 @@ def _keys(hashes: np.ndarray, lo: int = 0, hi: Optional[int] = None) -> List[byt
     return [raw[i:i + DIGEST] for i in range(0, len(raw), DIGEST)]
 
 
+NO_DEPTH = 0xFFFFFFFF
+
+
 class Table:
-    """The cache as a set of 32-byte keys.  No capacity limit, no eviction."""
+    """The cache as a set of 32-byte keys, with the recency state that
+    maintenance uses (the paper is silent on maintenance; the readings here
+    are listed in the design notes):
+
+    * a clock that advances by one with every insert or admission call;
+    * per key a stamp, the clock of the latest such call whose batch held
+      it, and a depth, the smallest block position (row within its request)
+      it had in that call;
+    * evict(max_keys) keeps the largest set of whole rank classes, ranked by
+      stamp (newest first) and then depth (shallowest first), that fits in
+      max_keys.  A chain's earlier block always has a stamp at least that of
+      a later block and a smaller depth, so the kept set stays prefix-closed;
+    * erase(keys) removes exactly the given keys."""
 
     def __init__(self):
         self.keys = set()
+        self.clock = 0
+        self.stamp = {}
+        self.depth = {}
+
+    def _touch(self, hashes: np.ndarray, blk_offsets) -> None:
+        self.clock += 1
+        blk_offsets = np.asarray(blk_offsets, dtype=np.int64)
+        pos = {}
+        for r in range(blk_offsets.shape[0] - 1):
+            a, b = int(blk_offsets[r]), int(blk_offsets[r + 1])
+            for j, k in enumerate(_keys(hashes, a, b)):
+                pos[k] = min(pos.get(k, NO_DEPTH), j)
+        for k, j in pos.items():
+            self.stamp[k] = self.clock
+            self.depth[k] = j
 
     def insert(self, hashes: np.ndarray, blk_offsets=None) -> int:
-        """T <- T u {every key of the batch}; returns how many were not in T."""
+        """T <- T u {every key of the batch}; returns how many were not in T.
+        Without offsets the batch is one request."""
         if blk_offsets is not None:
             blk_offsets = np.asarray(blk_offsets, dtype=np.int64)
             lo, hi = int(blk_offsets[0]), int(blk_offsets[-1])
         else:
             lo, hi = 0, int(hashes.shape[0])
+            blk_offsets = np.array([0, hi], dtype=np.int64)
         new = set(_keys(hashes, lo, hi)) - self.keys
         self.keys |= new
+        self._touch(hashes, blk_offsets)
         return len(new)
+
+    def rank(self, k: bytes):
+        return (self.stamp.get(k, 0), -self.depth.get(k, NO_DEPTH))
+
+    def evict(self, max_keys: int) -> int:
+        """Keeps the top rank classes that fit in max_keys; returns the
+        number of keys kept."""
+        classes = {}
+        for k in self.keys:
+            classes.setdefault(self.rank(k), []).append(k)
+        kept = set()
+        for rk in sorted(classes, reverse=True):
+            if len(kept) + len(classes[rk]) > max_keys:
+                break
+            kept |= set(classes[rk])
+        self.erase_set(self.keys - kept)
+        return len(kept)
+
+    def erase_set(self, ks) -> int:
+        gone = set(ks) & self.keys
+        self.keys -= gone
+        for k in gone:
+            self.stamp.pop(k, None)
+            self.depth.pop(k, None)
+        return len(gone)
+
+    def erase(self, hashes: np.ndarray) -> int:
+        """T <- T minus the given keys; returns how many were in T."""
+        return self.erase_set(_keys(hashes))
 
     def lookup(self, hashes: np.ndarray, blk_offsets) -> np.ndarray:
         """hit[r] = first j with h_j(r) not in T, or n_full(r) if none is missing."""
@@ -259,6 +321,7 @@ class Table:
             fresh = set(keys_r) - self.keys
             new[r] = len(fresh)
             self.keys |= fresh
+        self._touch(hashes, blk_offsets)
         return hits, new
 
 

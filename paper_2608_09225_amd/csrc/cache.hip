@@ -52,7 +52,8 @@ namespace kvgov {
 // ---------------------------------------------------------------------------
 
 __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long long *tags,
-                                                    int64_t slots, CacheMeta *m) {
+                                                    unsigned long long *rank, int64_t slots,
+                                                    CacheMeta *m) {
   const int64_t stride = (int64_t)gridDim.x * 256;
   const u32x4 ones = u32x4{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
   if (blockIdx.x == 0) {
@@ -64,6 +65,7 @@ __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long l
     if (threadIdx.x == 0) {
       m->exported = 0;
       m->ones_tag = 0;
+      m->ones_rank = 0;
       m->status = 0;
       m->ones_present = 0;
     }
@@ -72,6 +74,7 @@ __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long l
     keys[2 * s] = ones;
     keys[2 * s + 1] = ones;
     tags[s] = 0;
+    rank[s] = 0;
   }
 }
 
@@ -154,7 +157,10 @@ __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hash
         if (r >= 1 && jj >= 0 && jj < b_r - b_p && b_p + jj >= lo)
           dup = key_eq(key, load_key(hashes + (b_p + jj) * 32));
         uint32_t code = kCodeDup;
-        if (!dup) added += insert_key<ADMIT>(t, key, f, lo, hashes, epoch, &code);
+        // the depth of the key: its row within its request (clamped; only
+        // malformed interior offsets put it outside [0, 2^31))
+        const uint32_t depth = (uint32_t)(jj < 0 ? 0 : (jj > 0x7FFFFFFF ? 0x7FFFFFFF : jj));
+        if (!dup) added += insert_key<ADMIT>(t, key, f, lo, hashes, epoch, &code, depth);
         if (ADMIT) codes[f] = code;
       }
       rc = __shfl(r, 63, 64);
@@ -358,6 +364,216 @@ __global__ __launch_bounds__(256) void k_export(TableView t, uint8_t *out, int64
   }
 }
 
+// ---------------------------------------------------------------------------
+// maintenance: eviction by recency rank, erase, and the rebuild both end in
+// ---------------------------------------------------------------------------
+
+// Eviction keeps every key whose recency word (newer stamp first, then
+// smaller depth) is at least a threshold chosen by a radix select over the
+// 64-bit words, 8 bits per pass.
+
+struct SelectState {
+  unsigned long long prefix;     // rank bits decided so far
+  unsigned long long threshold;  // keep rank >= threshold once done
+  long long budget;              // keys still allowed below the decided part
+  unsigned long long kept;       // keys copied out by the compaction
+  unsigned long long erased;     // keys marked by erase
+  int32_t level;                 // 8-bit digits decided
+  int32_t done;
+};
+
+constexpr int kRankBins = 256;
+
+// Histogram of the next digit of the ranks that match the decided prefix
+// (occupied slots and the all-0xFF key), per workgroup in LDS.
+__global__ __launch_bounds__(256) void k_rank_hist(TableView t, const SelectState *st,
+                                                   unsigned int *hist) {
+  __shared__ unsigned int h[kRankBins];
+  if (st->done) return;
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int level = st->level;
+  const unsigned long long prefix = st->prefix;
+  const int shift = 56 - 8 * level;
+  const int64_t slots = (int64_t)t.mask + 1;
+  for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < slots;
+       s += (int64_t)gridDim.x * 256) {
+    if (t.tags[s] == 0) continue;
+    const uint64_t r = t.rank[s];
+    if (level == 0 || (r >> (shift + 8)) == prefix) atomicAdd(&h[(r >> shift) & 255], 1u);
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0 && t.meta->ones_present) {
+    const uint64_t r = t.meta->ones_rank;
+    if (level == 0 || (r >> (shift + 8)) == prefix) atomicAdd(&h[(r >> shift) & 255], 1u);
+  }
+  __syncthreads();
+  if (h[threadIdx.x]) atomicAdd(&hist[threadIdx.x], h[threadIdx.x]);
+}
+
+// One workgroup: the digit at which the kept count crosses the budget (keys
+// with a higher digit are kept), or the end when everything left fits.
+// Leaves the histogram cleared for the next pass.
+__global__ __launch_bounds__(256) void k_rank_select(SelectState *st, unsigned int *hist) {
+  __shared__ unsigned long long c[kRankBins];
+  __shared__ unsigned long long total;
+  const int t = threadIdx.x;
+  c[t] = hist[t];
+  hist[t] = 0;
+  const int done = st->done;
+  const long long budget = st->budget;
+  const int level = st->level;
+  const unsigned long long prefix = st->prefix;
+  __syncthreads();
+  if (done) return;
+  unsigned long long above = 0;  // keys whose digit exceeds t
+  for (int u = t + 1; u < kRankBins; ++u) above += c[u];
+  if (t == 0) total = above + c[0];
+  __syncthreads();
+  const unsigned long long B = (unsigned long long)budget;
+  if (total <= B) {
+    if (t == 0) {
+      st->threshold = level == 0 ? 0ull : prefix << (64 - 8 * level);
+      st->done = 1;
+    }
+    return;
+  }
+  if (above <= B && B < above + c[t]) {  // exactly one digit
+    const unsigned long long p = (prefix << 8) | (unsigned long long)t;
+    st->budget = budget - (long long)above;
+    st->prefix = p;
+    st->level = level + 1;
+    if (level + 1 == 8) {  // the whole class p does not fit: keep what ranks above it
+      st->threshold = p + 1;
+      st->done = 1;
+    }
+  }
+}
+
+__global__ void k_select_init(SelectState *st, unsigned int *hist, long long budget,
+                              int erase) {
+  if (threadIdx.x == 0) {
+    st->prefix = 0;
+    st->threshold = 0;  // erase: keep every key not marked
+    st->budget = budget;
+    st->kept = 0;
+    st->erased = 0;
+    st->level = 0;
+    st->done = erase;
+  }
+  hist[threadIdx.x] = 0;
+}
+
+// Erase: a present key's recency word becomes kErased (counted once per key).
+__global__ __launch_bounds__(256) void k_erase_mark(TableView t, const uint8_t *keys,
+                                                    int64_t n, SelectState *st) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const Key k = load_key(keys + i * 32);
+  unsigned long long *w = nullptr;
+  if (key_is_empty_pattern(k)) {
+    if (t.meta->ones_present) w = &t.meta->ones_rank;
+  } else {
+    const int64_t slot = find_slot(t, k);
+    if (slot >= 0) w = &t.rank[slot];
+  }
+  if (w && atomicExch(w, kErased) != kErased) atomicAdd(&st->erased, 1ull);
+}
+
+// Copies the kept keys and their recency to scratch (one atomic per wave).
+__global__ __launch_bounds__(256) void k_compact(TableView t, SelectState *st, u32x4 *out_keys,
+                                                 unsigned long long *out_rank, int64_t cap) {
+  const int64_t slots = (int64_t)t.mask + 1;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const unsigned long long thr = st->threshold;
+  const int lane = threadIdx.x & 63;
+  // every lane of a wave runs the same number of rounds (ballot inside);
+  // round -1 is the all-0xFF key, on lane 0 of the first wave
+  const int64_t rounds = (slots + stride - 1) / stride;
+  for (int64_t k = (gid < 64 ? -1 : 0); k < rounds; ++k) {
+    bool have = false;
+    unsigned long long r = 0;
+    u32x4 lo{}, hi{};
+    if (k < 0) {
+      r = t.meta->ones_rank;
+      have = gid == 0 && t.meta->ones_present && r != kErased && r >= thr;
+      lo = hi = u32x4{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+    } else {
+      const int64_t s = gid + k * stride;
+      if (s < slots && t.tags[s] != 0) {
+        r = t.rank[s];
+        if (r != kErased && r >= thr) {
+          have = true;
+          lo = t.keys[2 * s];
+          hi = t.keys[2 * s + 1];
+        }
+      }
+    }
+    const uint64_t mask = __ballot(have);
+    if (!mask) continue;
+    const int leader = __builtin_ctzll(mask);
+    unsigned long long base = 0;
+    if (lane == leader) base = atomicAdd(&st->kept, (unsigned long long)__popcll(mask));
+    base = __shfl(base, leader, 64);
+    if (have) {
+      const int64_t at = (int64_t)base + __popcll(mask & ((1ull << lane) - 1ull));
+      if (at < cap) {
+        out_keys[2 * at] = lo;
+        out_keys[2 * at + 1] = hi;
+        out_rank[at] = r;
+      }
+    }
+  }
+}
+
+// Empties the slots and the key counters for the rebuild; the latched error
+// and the export count stay.
+__global__ __launch_bounds__(256) void k_rebuild_fill(TableView t) {
+  const int64_t slots = (int64_t)t.mask + 1;
+  const u32x4 ones = u32x4{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+  if (blockIdx.x == 0) {
+    CacheMeta *m = t.meta;
+    for (int i = threadIdx.x; i < kCounterLanes; i += blockDim.x) {
+      m->n_keys[i] = 0;
+      m->new_keys[0][i] = 0;
+      m->new_keys[1][i] = 0;
+    }
+    if (threadIdx.x == 0) {
+      m->ones_tag = 0;
+      m->ones_rank = 0;
+      m->ones_present = 0;
+    }
+  }
+  for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < slots;
+       s += (int64_t)gridDim.x * 256) {
+    t.keys[2 * s] = ones;
+    t.keys[2 * s + 1] = ones;
+    t.tags[s] = 0;
+    t.rank[s] = 0;
+  }
+}
+
+// Inserts the kept keys again (all distinct) and restores their recency.
+__global__ __launch_bounds__(256) void k_reinsert(TableView t, const SelectState *st,
+                                                  const uint8_t *keys,
+                                                  const unsigned long long *rank,
+                                                  uint32_t epoch) {
+  __shared__ uint32_t lds4[4];
+  const int64_t n = (int64_t)st->kept;
+  uint32_t added = 0;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * 256) {
+    uint32_t code = kCodeFailed;
+    added += insert_key<false>(t, load_key(keys + i * 32), i, 0, keys, epoch, &code);
+    unsigned long long *dst =
+        code == kCodeOnes ? &t.meta->ones_rank : (code < kCodeFailed ? &t.rank[code] : nullptr);
+    if (dst) *dst = rank[i];
+  }
+  const uint32_t total = block_sum(added, lds4);
+  if (threadIdx.x == 0 && total)
+    atomicAdd(&t.meta->n_keys[blockIdx.x % kCounterLanes], (unsigned long long)total);
+}
+
 }  // namespace kvgov
 
 using namespace kvgov;
@@ -377,7 +593,7 @@ unsigned grid_for(int64_t work, int per_cu) {
 
 int enqueue_clear(kvgov_cache *c, hipStream_t s) {
   hipLaunchKernelGGL(k_cache_fill, dim3(grid_for(c->slots, 64)), dim3(256), 0, s, c->view.keys,
-                     c->view.tags, c->slots, c->view.meta);
+                     c->view.tags, c->view.rank, c->slots, c->view.meta);
   c->epoch.store(0);
   return launch_status();
 }
@@ -394,6 +610,62 @@ int read_meta(kvgov_cache *c, CacheMeta *m, hipStream_t s) {
     return KVGOV_E_HIP;
   if (hipStreamSynchronize(s) != hipSuccess) return KVGOV_E_HIP;
   return KVGOV_OK;
+}
+
+// Maintenance scratch, stream-ordered: selection state, the rank histogram
+// and room for every key of the table (32 B key + 8 B recency each).
+struct MaintScratch {
+  SelectState *st = nullptr;
+  unsigned int *hist = nullptr;
+  u32x4 *keys = nullptr;
+  unsigned long long *rank = nullptr;
+  void *base = nullptr;
+  int64_t cap = 0;
+};
+
+int maint_alloc(kvgov_cache *c, hipStream_t s, MaintScratch &m) {
+  m.cap = c->slots + 1;
+  const size_t off_hist = 256;
+  const size_t off_keys = off_hist + kRankBins * sizeof(unsigned int);
+  const size_t off_rank = off_keys + (size_t)m.cap * 32;
+  const size_t bytes = off_rank + (size_t)m.cap * 8;
+  if (hipMallocAsync(&m.base, bytes, s) != hipSuccess) return KVGOV_E_NOMEM;
+  uint8_t *b = static_cast<uint8_t *>(m.base);
+  m.st = reinterpret_cast<SelectState *>(b);
+  m.hist = reinterpret_cast<unsigned int *>(b + off_hist);
+  m.keys = reinterpret_cast<u32x4 *>(b + off_keys);
+  m.rank = reinterpret_cast<unsigned long long *>(b + off_rank);
+  return KVGOV_OK;
+}
+
+// Copies out what ranks at or above the selected threshold, empties the
+// table and inserts the copies again; then reads one counter if asked
+// (waiting for the stream) and frees the scratch in stream order.
+int compact_rebuild(kvgov_cache *c, hipStream_t s, MaintScratch &m, const unsigned long long *count,
+                    int64_t *out) {
+  const uint32_t epoch = c->epoch.fetch_add(1) + 1;
+  int rc = epoch == 0xFFFFFFFFu ? KVGOV_E_UNSUPPORTED : KVGOV_OK;
+  if (rc == KVGOV_OK) {
+    hipLaunchKernelGGL(k_compact, dim3(grid_for(c->slots, 32)), dim3(256), 0, s, c->view, m.st,
+                       m.keys, m.rank, m.cap);
+    hipLaunchKernelGGL(k_rebuild_fill, dim3(grid_for(c->slots, 64)), dim3(256), 0, s, c->view);
+    hipLaunchKernelGGL(k_reinsert, dim3(grid_for(m.cap, 16)), dim3(256), 0, s, c->view, m.st,
+                       reinterpret_cast<const uint8_t *>(m.keys), m.rank, epoch);
+    rc = launch_status();
+  }
+  unsigned long long host = 0;
+  if (rc == KVGOV_OK && out &&
+      hipMemcpyAsync(&host, count, sizeof host, hipMemcpyDeviceToHost, s) != hipSuccess)
+    rc = KVGOV_E_HIP;
+  if (hipFreeAsync(m.base, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
+  if (rc == KVGOV_OK && out) {
+    if (hipStreamSynchronize(s) != hipSuccess) return KVGOV_E_HIP;
+    *out = (int64_t)host;
+    CacheMeta meta{};
+    rc = read_meta(c, &meta, s);
+    if (rc == KVGOV_OK) rc = meta.status;
+  }
+  return rc;
 }
 
 // Keys added by insert call `epoch` (waits for the stream), and the latched
@@ -434,18 +706,22 @@ int kvgov_cache_create(int32_t log2_slots, kvgov_cache **out) {
   c->log2_slots = log2_slots;
   c->slots = (int64_t)1 << log2_slots;
   c->view.mask = (uint64_t)c->slots - 1;
-  void *keys = nullptr, *tags = nullptr, *meta = nullptr;
+  void *keys = nullptr, *tags = nullptr, *rank = nullptr, *meta = nullptr;
   if (hipMalloc(&keys, (size_t)c->slots * 32) != hipSuccess ||
       hipMalloc(&tags, (size_t)c->slots * 8) != hipSuccess ||
+      hipMalloc(&rank, (size_t)c->slots * 8) != hipSuccess ||
       hipMalloc(&meta, sizeof(CacheMeta)) != hipSuccess) {
     if (keys) (void)hipFree(keys);
     if (tags) (void)hipFree(tags);
+    if (rank) (void)hipFree(rank);
     if (meta) (void)hipFree(meta);
     delete c;
     return KVGOV_E_NOMEM;
   }
   c->view.keys = static_cast<u32x4 *>(keys);
   c->view.tags = static_cast<unsigned long long *>(tags);
+  c->view.rank = static_cast<unsigned long long *>(rank);
+  c->view.track = 0;
   c->view.meta = static_cast<CacheMeta *>(meta);
   int rc = enqueue_clear(c, nullptr);
   if (rc == KVGOV_OK && hipStreamSynchronize(nullptr) != hipSuccess) rc = KVGOV_E_HIP;
@@ -463,6 +739,7 @@ int kvgov_cache_destroy(kvgov_cache *c) {
   if (hipDeviceSynchronize() != hipSuccess) rc = KVGOV_E_HIP;
   if (hipFree(c->view.keys) != hipSuccess) rc = KVGOV_E_HIP;
   if (hipFree(c->view.tags) != hipSuccess) rc = KVGOV_E_HIP;
+  if (hipFree(c->view.rank) != hipSuccess) rc = KVGOV_E_HIP;
   if (hipFree(c->view.meta) != hipSuccess) rc = KVGOV_E_HIP;
   delete c;
   return rc;
@@ -582,6 +859,48 @@ int kvgov_cache_admit(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_
   if (hipFreeAsync(codes, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
   if (rc != KVGOV_OK || !n_new) return rc;
   return read_new_keys(c, epoch, n_new, s);
+}
+
+int kvgov_cache_set_recency(kvgov_cache *c, int32_t on) {
+  if (!c || (on != 0 && on != 1)) return KVGOV_E_INVAL;
+  c->view.track = (uint32_t)on;
+  return KVGOV_OK;
+}
+
+int kvgov_cache_evict(kvgov_cache *c, int64_t max_keys, int64_t *n_kept, void *stream) {
+  if (!c || max_keys < 0) return KVGOV_E_INVAL;
+  if (!c->view.track) return KVGOV_E_UNSUPPORTED;
+  int rc = check_device(c);
+  if (rc != KVGOV_OK) return rc;
+  hipStream_t s = as_stream(stream);
+  MaintScratch m;
+  rc = maint_alloc(c, s, m);
+  if (rc != KVGOV_OK) return rc;
+  hipLaunchKernelGGL(k_select_init, dim3(1), dim3(kRankBins), 0, s, m.st, m.hist,
+                     (long long)max_keys, 0);
+  for (int level = 0; level < 8; ++level) {
+    hipLaunchKernelGGL(k_rank_hist, dim3(grid_for(c->slots, 16)), dim3(256), 0, s, c->view,
+                       m.st, m.hist);
+    hipLaunchKernelGGL(k_rank_select, dim3(1), dim3(kRankBins), 0, s, m.st, m.hist);
+  }
+  return compact_rebuild(c, s, m, &m.st->kept, n_kept);
+}
+
+int kvgov_cache_erase(kvgov_cache *c, const uint8_t *keys, int64_t n_keys, int64_t *n_erased,
+                      void *stream) {
+  if (!c || n_keys < 0 || (n_keys > 0 && !keys)) return KVGOV_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(keys) & 3) return KVGOV_E_INVAL;
+  int rc = check_device(c);
+  if (rc != KVGOV_OK) return rc;
+  hipStream_t s = as_stream(stream);
+  MaintScratch m;
+  rc = maint_alloc(c, s, m);
+  if (rc != KVGOV_OK) return rc;
+  hipLaunchKernelGGL(k_select_init, dim3(1), dim3(kRankBins), 0, s, m.st, m.hist, 0ll, 1);
+  if (n_keys > 0)
+    hipLaunchKernelGGL(k_erase_mark, dim3((unsigned)ceil_div(n_keys, 256)), dim3(256), 0, s,
+                       c->view, keys, n_keys, m.st);
+  return compact_rebuild(c, s, m, &m.st->erased, n_erased);
 }
 
 int kvgov_cache_count(kvgov_cache *c, int64_t *n_keys, void *stream) {

@@ -119,7 +119,7 @@ __global__ __launch_bounds__(256) void k_radix_roots(TableView t, const uint8_t 
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count;
        i += (int64_t)gridDim.x * 256) {
     uint32_t code;
-    added += insert_key<false>(t, load_key(keys + i * 32), i, 0, keys, epoch, &code);
+    added += insert_key<false>(t, load_key(keys + i * 32), i, 0, keys, epoch, &code, 0u);
   }
   if (added) atomicAdd(&t.meta->n_keys[blockIdx.x % kCounterLanes], (unsigned long long)added);
 }

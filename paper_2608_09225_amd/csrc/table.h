@@ -21,15 +21,28 @@ struct CacheMeta {
   unsigned long long new_keys[2][kCounterLanes];  // keys added by insert call `epoch`, at [epoch & 1]
   unsigned long long exported;                    // keys written by the latest export
   unsigned long long ones_tag;                    // the all-0xFF key's tag (0 = absent)
+  unsigned long long ones_rank;                   // its recency rank (as `rank`)
   int32_t status;                                 // latched error (0 = none)
   int32_t ones_present;                           // the all-0xFF key is in the table
 };
 
+// Recency of a key (table maintenance, when the table tracks it): one word,
+// (stamp << 32) | (kNoDepth - depth), where the stamp is the epoch of the
+// latest insert or admission call whose batch held the key and the depth
+// the smallest row position (within its request) the key had in that call.
+// Newer calls rank higher, and within a call shallower positions; both are
+// raised by one atomicMax.  0 = never touched; kErased marks a key an erase
+// call is removing.
+constexpr uint32_t kNoDepth = 0xFFFFFFFFu;
+constexpr unsigned long long kErased = ~0ull;
+
 struct TableView {
   u32x4 *keys;  // 2 per slot
   unsigned long long *tags;
+  unsigned long long *rank;  // recency word per slot
   CacheMeta *meta;
-  uint64_t mask;  // slots - 1
+  uint64_t mask;   // slots - 1
+  uint32_t track;  // inserts and admissions raise `rank`
 };
 
 struct Key {
@@ -88,27 +101,50 @@ __device__ __forceinline__ void lower_claim(unsigned long long *tag, unsigned lo
   if (mine < seen) atomicMin(tag, mine);
 }
 
+// Raises a key's recency word to `mine`.  The word only grows within a
+// call, so a plain read (possibly a stale line of this XCD's L2) that already
+// shows `mine` or more ends it; otherwise a device-coherent read, and an
+// atomic only where it changes something: a hot key held by thousands of
+// rows costs a few atomics.  The row that just claimed the slot goes
+// straight to the atomic.
+__device__ __forceinline__ void touch(unsigned long long *w, unsigned long long mine,
+                                      bool claimed) {
+  if (!claimed) {
+    if (*w >= mine) return;
+    if (__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= mine) return;
+  }
+  atomicMax(w, mine);
+}
+
+__device__ __forceinline__ unsigned long long recency(uint32_t epoch, uint32_t depth) {
+  return ((unsigned long long)epoch << 32) | (unsigned long long)(kNoDepth - depth);
+}
+
 // Tags only ever change from 0 to a claim (and, within the claiming call, to
 // a smaller claim of the same key), so a plain (possibly stale) read can only
 // show 0 for a claimed slot; the compare-and-swap that follows then fails
 // and returns the claim.  Coherent atomics are used for the claim only.
-// Returns 1 if the key was added; *code receives where the key went.
+// Returns 1 if the key was added; *code receives where the key went.  On a
+// table that tracks recency the key (added or found) is touched with
+// (epoch, depth) unless depth is kNoDepth.
 template <bool ADMIT>
 __device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &key, int64_t i,
                                                int64_t lo, const uint8_t *hashes,
-                                               uint32_t epoch, uint32_t *code) {
+                                               uint32_t epoch, uint32_t *code,
+                                               uint32_t depth = kNoDepth) {
   const unsigned long long mine = ((unsigned long long)epoch << 32) |
                                   (unsigned long long)(i - lo + 1);
   if (key_is_empty_pattern(key)) {
     *code = kCodeOnes;
     unsigned long long expect = 0;
-    if (__hip_atomic_compare_exchange_strong(&t.meta->ones_tag, &expect, mine, __ATOMIC_RELAXED,
-                                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-      atomicExch(&t.meta->ones_present, 1);
-      return 1;
-    }
-    if (ADMIT && (uint32_t)(expect >> 32) == epoch) lower_claim(&t.meta->ones_tag, expect, mine);
-    return 0;
+    const bool won = __hip_atomic_compare_exchange_strong(
+        &t.meta->ones_tag, &expect, mine, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+        __HIP_MEMORY_SCOPE_AGENT);
+    if (won) atomicExch(&t.meta->ones_present, 1);
+    if (!won && ADMIT && (uint32_t)(expect >> 32) == epoch)
+      lower_claim(&t.meta->ones_tag, expect, mine);
+    if (t.track && depth != kNoDepth) touch(&t.meta->ones_rank, recency(epoch, depth), won);
+    return won ? 1u : 0u;
   }
   uint64_t s = slot_hash(key) & t.mask;
   for (uint64_t probes = 0; probes <= t.mask; ++probes) {
@@ -120,6 +156,7 @@ __device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &ke
         t.keys[2 * s] = key.lo;
         t.keys[2 * s + 1] = key.hi;
         *code = (uint32_t)s;
+        if (t.track && depth != kNoDepth) touch(&t.rank[s], recency(epoch, depth), true);
         return 1;
       }
       tag = expect;  // somebody claimed it first: examine the claimant
@@ -135,6 +172,7 @@ __device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &ke
     if (key_eq(key, other)) {
       if (ADMIT && current) lower_claim(&t.tags[s], tag, mine);
       *code = (uint32_t)s;
+      if (t.track && depth != kNoDepth) touch(&t.rank[s], recency(epoch, depth), false);
       return 0;
     }
     s = (s + 1) & t.mask;
@@ -193,7 +231,7 @@ struct kvgov_cache {
   int device;
   int32_t log2_slots;
   int64_t slots;
-  kvgov::TableView view;
+  kvgov::TableView view;  // view.track: recency tracking on
   std::atomic<uint32_t> epoch;
 };
 

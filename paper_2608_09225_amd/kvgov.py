@@ -13,7 +13,8 @@ Calls mirror the C ABI one to one:
     kvgov_hash_chains   -> hash_chains(tokens, tok_offsets, principal, salts, mode, ...)
     kvgov_hash_chains_resume -> hash_chains_resume(..., start_block, parents, ...)
     kvgov_resume_offsets -> resume_offsets(tok_offsets, start_block)
-    kvgov_cache_*       -> Cache(log2_slots).insert / lookup / admit / clear / count / export
+    kvgov_cache_*       -> Cache(log2_slots).insert / lookup / admit / set_recency / evict /
+                           erase / clear / count / export
     kvgov_radix_*       -> Radix(log2_block_slots, log2_edge_slots).insert / match / clear / stats
 """
 from __future__ import annotations
@@ -64,6 +65,9 @@ _SIGNATURES = {
                                          _c_i32, _vp, _vp, _c_i64, _vp, _vp]),
     "kvgov_radix_stats": (ctypes.c_int, [_vp, ctypes.POINTER(_c_i64), ctypes.POINTER(_c_i64),
                                          _vp]),
+    "kvgov_cache_set_recency": (ctypes.c_int, [_vp, _c_i32]),
+    "kvgov_cache_evict": (ctypes.c_int, [_vp, _c_i64, ctypes.POINTER(_c_i64), _vp]),
+    "kvgov_cache_erase": (ctypes.c_int, [_vp, _vp, _c_i64, ctypes.POINTER(_c_i64), _vp]),
     "kvgov_cache_count": (ctypes.c_int, [_vp, ctypes.POINTER(_c_i64), _vp]),
     "kvgov_cache_export": (ctypes.c_int, [_vp, _vp, _c_i64, ctypes.POINTER(_c_i64), _vp]),
 }
@@ -356,6 +360,30 @@ class Cache:
                                        ctypes.byref(nn) if sync else None, _stream(stream)),
                "kvgov_cache_admit")
         return hits, new, (int(nn.value) if sync else None)
+
+    def set_recency(self, on: bool = True):
+        """Tracks recency (needed by evict) from the next insert on."""
+        _check(lib().kvgov_cache_set_recency(self.handle, 1 if on else 0),
+               "kvgov_cache_set_recency")
+
+    def evict(self, max_keys: int, sync: bool = True, stream=None) -> Optional[int]:
+        """Keeps the most recent rank classes that fit in max_keys; with
+        ``sync`` returns the number of keys kept."""
+        v = _c_i64(-1)
+        _check(lib().kvgov_cache_evict(self.handle, int(max_keys),
+                                       ctypes.byref(v) if sync else None, _stream(stream)),
+               "kvgov_cache_evict")
+        return int(v.value) if sync else None
+
+    def erase(self, keys: torch.Tensor, sync: bool = True, stream=None) -> Optional[int]:
+        """Removes the given keys (uint8 [n, 32]); with ``sync`` returns how
+        many of them were present."""
+        ks = _dev(keys, torch.uint8, "keys")
+        v = _c_i64(-1)
+        _check(lib().kvgov_cache_erase(self.handle, _ptr(ks), ks.shape[0] if ks.dim() else 0,
+                                       ctypes.byref(v) if sync else None, _stream(stream)),
+               "kvgov_cache_erase")
+        return int(v.value) if sync else None
 
     def count(self, stream=None) -> int:
         v = _c_i64()

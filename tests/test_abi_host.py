@@ -118,6 +118,9 @@ def test_host_validation_returns_before_any_launch():
     assert L.kvgov_cache_insert(None, fake, fake, 1, 4, None, None) == INVAL
     assert L.kvgov_cache_lookup(None, fake, fake, 1, 4, fake, None) == INVAL
     assert L.kvgov_cache_admit(None, fake, fake, 1, 4, fake, fake, None, None) == INVAL
+    assert L.kvgov_cache_set_recency(None, 1) == INVAL
+    assert L.kvgov_cache_evict(None, 10, None, None) == INVAL
+    assert L.kvgov_cache_erase(None, fake, 1, None, None) == INVAL
     # radix
     assert L.kvgov_radix_create(3, 10, ctypes.byref(h)) == INVAL
     assert L.kvgov_radix_create(10, 31, ctypes.byref(h)) == INVAL

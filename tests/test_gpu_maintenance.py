@@ -1,0 +1,165 @@
+"""GPU parity of table maintenance (kvgov_cache_evict / kvgov_cache_erase)
+against the oracle's Table: after every step of a history of inserts,
+admissions, evictions and erasures, the exported key set, the counts and
+later lookups are compared exactly."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from tests.test_oracle_maintenance import K as key_of, arr, _chains, _batch
+
+pytestmark = pytest.mark.gpu
+
+KV = pytest.importorskip("paper_2608_09225_amd.kvgov")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    KV.lib()
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def dev(x):
+    return torch.from_numpy(np.require(x, requirements=["C", "W"])).cuda()
+
+
+def key_set(t):
+    a = t.cpu().numpy()
+    return {a[i].tobytes() for i in range(a.shape[0])}
+
+
+def replay(hist, log2_slots=16, probes=None):
+    """Runs `hist` on a GPU table and on the oracle, checking after each step."""
+    T = O.Table()
+    with KV.Cache(log2_slots) as c:
+        c.set_recency(True)
+        for op, x in hist:
+            if op == "insert":
+                h, bo = x
+                assert c.insert(dev(h), dev(bo)) == T.insert(h, bo)
+            elif op == "admit":
+                h, bo = x
+                hits, new, n_new = c.admit(dev(h), dev(bo))
+                wh, wn = T.admit(h, bo)
+                assert np.array_equal(hits.cpu().numpy(), wh)
+                assert np.array_equal(new.cpu().numpy(), wn)
+            elif op == "evict":
+                assert c.evict(x) == T.evict(x), ("evict", x)
+            else:
+                assert c.erase(dev(x)) == T.erase(x), "erase"
+            assert key_set(c.export()) == T.keys, op
+            assert c.count() == len(T.keys)
+        if probes is not None:
+            h, bo = probes
+            assert np.array_equal(c.lookup(dev(h), dev(bo)).cpu().numpy(), T.lookup(h, bo))
+    return T
+
+
+def test_hand_built_history():
+    a = [key_of(i) for i in range(10)]
+    one = np.array([0, 3], np.int64)
+    base = [("insert", (arr(a[0:3]), one)),
+            ("insert", (arr([a[0], a[3], a[4]]), one)),
+            ("insert", (arr([a[5], a[1]]), np.array([0, 1, 2], np.int64)))]
+    for max_keys in (0, 1, 2, 3, 4, 5, 6, 100):
+        replay(base + [("evict", max_keys)])
+    replay(base + [("erase", arr([a[1], a[7], a[1]]))])
+    T = replay(base + [("evict", 2), ("insert", (arr([a[2]]), np.array([0, 1], np.int64))),
+                       ("evict", 1)])
+    assert T.keys == {a[2]}
+
+
+def test_chain_history_with_admissions():
+    chains = _chains(3, 160)
+    g = np.random.default_rng(4)
+    hist = []
+    for i in range(0, 160, 16):
+        hist.append(("insert" if i % 32 else "admit", _batch(chains[i:i + 16])))
+        if i % 48 == 0:
+            idx = g.integers(0, i + 1, 9)
+            hist.append(("insert", _batch([chains[j] for j in idx])))
+        if i % 64 == 32:
+            hist.append(("evict", int(g.integers(50, 600))))
+    hist.append(("evict", 250))
+    hist.append(("insert", _batch(chains[:20])))
+    hist.append(("erase", arr([k for c in chains[20:40] for k in c[:2]])))
+    hist.append(("admit", _batch(chains[40:80])))
+    T = replay(hist, probes=_batch(chains))
+    # prefix closure of what the last eviction kept, among chains inserted whole
+    assert len(T.keys) > 0
+
+
+def test_arbitrary_keys_repeats_and_all_ff():
+    g = np.random.default_rng(5)
+    pool = [key_of(i) for i in range(300)] + [b"\xff" * 32]
+    hist = []
+    for step in range(8):
+        lens = g.integers(0, 9, 40)
+        bo = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+        rows = [pool[int(i)] for i in g.integers(0, len(pool), int(bo[-1]))]
+        hist.append(("insert" if step % 2 else "admit", (arr(rows), bo)))
+        if step % 3 == 2:
+            hist.append(("evict", int(g.integers(20, 200))))
+    hist.append(("erase", arr([pool[-1], pool[0], pool[0], key_of(999)])))
+    hist.append(("evict", 0))
+    replay(hist, log2_slots=12)
+
+
+def test_eviction_at_scale():
+    """~200k keys over 6 insert calls of whole chains; evictions to several
+    sizes, then the table keeps working (insert, lookup)."""
+    g = np.random.default_rng(6)
+    n = 6000
+    lens = g.integers(1, 60, n)
+    keys = g.integers(0, 256, (int(lens.sum()), 32), dtype=np.uint8)
+    keys[:, 0] = 7  # never the all-0xFF key
+    bo = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    hist = []
+    for k in range(6):
+        sel = np.arange(k * 1000, (k + 1) * 1000)
+        rows = np.concatenate([keys[bo[r]:bo[r + 1]] for r in sel])
+        sb = np.concatenate([[0], np.cumsum(lens[sel])]).astype(np.int64)
+        hist.append(("insert", (rows, sb)))
+    hist += [("evict", 150000), ("evict", 90000), ("evict", 90000), ("evict", 12345)]
+    hist.append(("insert", (keys[:bo[500]], bo[:501])))
+    replay(hist, log2_slots=19, probes=(keys, bo))
+
+
+def test_evict_and_erase_async_then_count():
+    g = np.random.default_rng(7)
+    h = g.integers(0, 256, (500, 32), dtype=np.uint8)
+    with KV.Cache(12) as c:
+        c.set_recency(True)
+        c.insert(dev(h), dev(np.array([0, 500], np.int64)))
+        assert c.evict(100, sync=False) is None
+        assert c.erase(dev(h[:10]), sync=False) is None
+        n = c.count()
+    T = O.Table()
+    T.insert(h, np.array([0, 500], np.int64))
+    T.evict(100)
+    T.erase(h[:10])
+    assert n == len(T.keys)
+
+
+def test_untracked_table_erases_but_does_not_evict():
+    c_ = KV.header_constants()
+    g = np.random.default_rng(8)
+    h = g.integers(0, 256, (300, 32), dtype=np.uint8)
+    bo = np.array([0, 300], np.int64)
+    with KV.Cache(12) as c:
+        c.insert(dev(h), dev(bo))
+        with pytest.raises(KV.KvgovError) as e:
+            c.evict(10)
+        assert e.value.code == c_["KVGOV_E_UNSUPPORTED"]
+        assert c.erase(dev(h[:40])) == 40
+        assert key_set(c.export()) == {h[i].tobytes() for i in range(40, 300)}
+        # switched on later: the tracked keys rank above the untracked ones
+        c.set_recency(True)
+        c.insert(dev(h[100:150]), dev(np.array([0, 50], np.int64)))
+        assert c.evict(50) == 50
+        assert key_set(c.export()) == {h[i].tobytes() for i in range(100, 150)}
