@@ -27,12 +27,15 @@ longest request hashed alone), the device's measured peaks (integer-VALU and
 those, and the CPU oracle per phase, on one core and with the host's CPU
 model and SHA extension flag.
 
---config {tiny,template,large,session,admission} runs the same kind of step
-on those workloads (large: chains + insert + a re-lookup of the inserted
-batch; session: turn-2 chains resumed at turn 1's last full block from its
-digest, insert and re-lookup of the new blocks, and the full rehash timed
-beside; admission: the paper-shaped chains, then one lookup-then-insert
-call over both batches in request order instead of insert + lookup);
+--config {tiny,template,large,session,admission,radix,maintenance} runs the
+same kind of step on those workloads (large: chains + insert + a re-lookup of
+the inserted batch; session: turn-2 chains resumed at turn 1's last full
+block from its digest, insert and re-lookup of the new blocks, and the full
+rehash timed beside; admission: the paper-shaped chains, then one
+lookup-then-insert call over both batches in request order instead of
+insert + lookup; radix: the radix index's insert of the insert batch and
+token-granular match of the re-lookup batch; maintenance: two tracked
+inserts, an eviction to half the keys, an erase, then the lookup);
 --config probe times lookups alone against the 8M-key resident table (the
 resident chains, the probe chains and the insert are done before timing).
 Only the default is the bench line; the others are for the per-config table.
@@ -88,6 +91,15 @@ RADIX_MATCH_BYTES_STEP = 12
 RADIX_INSERT_BYTES_RECORD = 32
 RADIX_INSERT_BYTES_EDGE = 12
 RADIX_EDGE_SLOTS_LOG2 = 23
+# Maintenance (evict, erase): per slot one scan of tag and recency word for
+# the ranks, the compaction scan (tag + word) and the refill (key, tag, word
+# written); per kept key its key read and 40 B written to scratch, then read
+# back, a probe's tag read and its key, tag and word written again.  Erase
+# marks: per listed key its 32 B, the slot key compared and the word swapped.
+EVICT_BYTES_PER_SLOT = 16 + 16 + 48
+ERASE_BYTES_PER_SLOT = 16 + 48
+MAINT_BYTES_PER_KEPT = 32 + 40 + 40 + 8 + 48
+ERASE_BYTES_PER_LISTED = 32 + 32 + 8
 # Admission: the insert's bytes, plus per row a 4-byte code written and read
 # back and an 8-byte tag read; per request two 8-byte offsets and two 4-byte
 # outputs.
@@ -105,6 +117,9 @@ DESCRIPTIONS = {
              "1M probes of U{{8..64}} blocks, 70% own-principal prefixes, 30% foreign",
     "large": "large batch: 65536 requests, lognormal lengths (median 2048, sigma 1, max "
              "32768 tokens), 4096 principals, root and boundary; chains + insert + re-lookup",
+    "maintenance": "paper-shaped batches on a recency-tracking table: insert batch then "
+                   "re-lookup batch (two insert calls), evict to half the keys, erase a tenth "
+                   "of the insert batch's rows, look up the re-lookup batch; root and boundary",
     "radix": "paper-shaped batches on the radix index: 4096 insert-batch sequences inserted, "
              "4096 re-lookup-batch requests matched token by token, 64 principals, root "
              "(per-principal trees) and unsalted; chains + clear + insert + match",
@@ -274,6 +289,8 @@ def cpu_baseline(wl: W.Workload, processes: int, max_blocks: int):
         return cpu_baseline_admission(wl, processes)
     if wl.name == "radix":
         return cpu_baseline_radix(wl, processes)
+    if wl.name == "maintenance":
+        return cpu_baseline_maintenance(wl, processes)
     same = wl.name == "large"
     A = capped(wl.insert, max_blocks)
     B = A if same else capped(wl.lookup, max_blocks)
@@ -330,6 +347,51 @@ def cpu_baseline(wl: W.Workload, processes: int, max_blocks: int):
                           f"{W.MODE_NAMES[wl.modes[0]]} mode",
                 "salts_us_per_key": cpu_salt_cost(wl) * 1e6,
             },
+            "host": host_cpu_info()}
+
+
+def cpu_baseline_maintenance(wl: W.Workload, processes: int):
+    """The oracle's step on the same workload: chains of both batches (over
+    worker processes), then in one process the two inserts, the eviction to
+    half the keys, the erase of a tenth of the insert batch's rows and the
+    lookup of the re-lookup batch."""
+    import oracle as O
+    A, B = wl.insert, wl.lookup
+    X = concat(A, B)
+    nA = int(A.block_counts().sum())
+    clock = time.perf_counter
+    t = {"salts": 0.0, "chains": 0.0, "insert": 0.0, "evict": 0.0, "erase": 0.0, "lookup": 0.0}
+    t0 = clock()
+    salts = O.salts(wl.K, wl.principal_ids)
+    t["salts"] = clock() - t0
+    tokens = 0
+    for mode in wl.modes:
+        t0 = clock()
+        h = O.hash_chains_parallel(X.tokens, X.tok_offsets, X.principal, salts, mode,
+                                   X.boundary_tok, processes=processes)
+        t["chains"] += clock() - t0
+        tokens += 16 * h.shape[0]
+        T = O.Table()
+        t0 = clock()
+        T.insert(h[:nA], A.blk_offsets())
+        T.insert(h[nA:], B.blk_offsets())
+        t["insert"] += clock() - t0
+        t0 = clock()
+        T.evict(int(len(T.keys) * wl.notes["evict_fraction"]))
+        t["evict"] += clock() - t0
+        t0 = clock()
+        T.erase(h[:int(nA * wl.notes["erase_fraction"])])
+        t["erase"] += clock() - t0
+        t0 = clock()
+        T.lookup(h[nA:], B.blk_offsets())
+        t["lookup"] += clock() - t0
+    dt = sum(t.values())
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": processes, "kind": "oracle",
+            "sample": (f"one full step of the same workload ({tokens} block tokens hashed, "
+                       f"{len(wl.modes)} modes) in {dt:.1f} s; chains over {processes} worker "
+                       "processes, the table steps in one process"),
+            "seconds": dt,
+            "phases": {k + "_s": v for k, v in t.items()},
             "host": host_cpu_info()}
 
 
@@ -599,6 +661,7 @@ def main():
     salts = torch.empty((wl.P, 32), dtype=torch.uint8, device=dev)
     status = K.new_status(dev)
     radix_cfg = wl.name == "radix"
+    maint_cfg = wl.name == "maintenance"
     caches = {m: K.Cache(wl.log2_slots) for m in modes} if not radix_cfg else {}
     radixes = {m: K.Radix(wl.log2_slots, RADIX_EDGE_SLOTS_LOG2) for m in modes} \
         if radix_cfg else {}
@@ -644,6 +707,23 @@ def main():
                           xx["boundary_tok"], blk_offsets=xx["blk_offsets"],
                           out=out[m] if out_ is None else out_, status=status, check=False,
                           stream=s)
+
+    ev_ins_b, ev_evict, ev_erase = [], [], []
+    max_keys, n_erase, new_a = {}, 0, {}
+    if maint_cfg:
+        # untimed set-up: the keys both inserts leave in the table fix the
+        # eviction target (half of them); the erase list is the first tenth
+        # of the insert batch's rows
+        K.salts(wl.K, ids, out=salts)
+        n_erase = int(nA * wl.notes["erase_fraction"])
+        for m in modes:
+            caches[m].set_recency(True)
+            hash_call(m, main_s)
+            new_a[m] = caches[m].insert(out[m][0:nA], boA)
+            caches[m].insert(out[m][nA:], boB)
+            max_keys[m] = int(caches[m].count() * wl.notes["evict_fraction"])
+            caches[m].clear()
+        torch.cuda.synchronize()
 
     probe_hash_ms = None
     if probe_only:
@@ -728,6 +808,20 @@ def main():
                     caches[m].insert(hA, boA, sync=False, stream=s)
                     if end:
                         end()
+                if maint_cfg:
+                    # the second insert call, then the maintenance calls
+                    end = timed(ev_ins_b, m, s) if record else None
+                    caches[m].insert(hB, boB, sync=False, stream=s)
+                    if end:
+                        end()
+                    end = timed(ev_evict, m, s) if record else None
+                    caches[m].evict(max_keys[m], sync=False, stream=s)
+                    if end:
+                        end()
+                    end = timed(ev_erase, m, s) if record else None
+                    caches[m].erase(hA[:n_erase], sync=False, stream=s)
+                    if end:
+                        end()
             if not admission and not radix_cfg:
                 if record:
                     l0 = torch.cuda.Event(enable_timing=True)
@@ -775,6 +869,25 @@ def main():
         got_new = {m: adm_new[m].cpu().numpy() for m in modes}
         gates["G4_new_blocks_by_construction"] = all(
             bool(np.array_equal(got_new[m], X.block_counts() - exp[m])) for m in modes)
+    if maint_cfg:
+        # the table after the last step, replayed by the oracle: both inserts,
+        # the eviction, the erase; then the re-lookup batch and the count
+        exp = None
+        import oracle as O
+        osl = O.salts(wl.K, wl.principal_ids)
+        okm = True
+        for m in modes:
+            ho = O.hash_chains_parallel(X.tokens, X.tok_offsets, X.principal, osl, m,
+                                        X.boundary_tok,
+                                        processes=min(16, len(os.sched_getaffinity(0))))
+            T = O.Table()
+            T.insert(ho[:nA], A.blk_offsets())
+            T.insert(ho[nA:], B.blk_offsets())
+            T.evict(max_keys[m])
+            T.erase(ho[:n_erase])
+            okm &= n_keys[W.MODE_NAMES[m]] == len(T.keys)
+            okm &= bool(np.array_equal(got_hits[m], T.lookup(ho[nA:], B.blk_offsets())))
+        gates["G4_maintained_state_matches_oracle"] = bool(okm)
     if radix_cfg:
         exp = None
         got_match = {m: matched[m].cpu().numpy() for m in modes}
@@ -1021,10 +1134,27 @@ def main():
                                  "gbs": look_bytes[m] / sec / 1e9}
             phases[W.MODE_NAMES[m]] = ph
             continue
+        if maint_cfg:
+            slots = 1 << wl.log2_slots
+            kept = max_keys[m]  # an upper bound of the keys the eviction keeps
+            st = stats(per(ev_ins_b)[m])
+            ph["insert_b"] = {**st, "keys": nX - nA,
+                              "keys_per_s": (nX - nA) / (st["ms_median"] * 1e-3)}
+            st = stats(per(ev_evict)[m])
+            b = EVICT_BYTES_PER_SLOT * slots + MAINT_BYTES_PER_KEPT * kept
+            ph["evict"] = {**st, "slots": slots, "max_keys": kept, "algorithmic_bytes": b,
+                           "gbs": b / (st["ms_median"] * 1e-3) / 1e9}
+            st = stats(per(ev_erase)[m])
+            b = (ERASE_BYTES_PER_SLOT * slots + MAINT_BYTES_PER_KEPT * n_keys[W.MODE_NAMES[m]] +
+                 ERASE_BYTES_PER_LISTED * n_erase)
+            ph["erase"] = {**st, "listed_keys": n_erase, "algorithmic_bytes": b,
+                           "gbs": b / (st["ms_median"] * 1e-3) / 1e9}
         if not probe_only:
             st = stats(ins_t[m])
             sec = st["ms_median"] * 1e-3
             n_new = n_keys[W.MODE_NAMES[m]]
+            if maint_cfg:
+                n_new = new_a[m]  # the insert batch's new keys, from the set-up run
             ibytes = INSERT_BYTES_NEW * n_new + INSERT_BYTES_PRESENT * (nA - n_new)
             ph["insert"] = {**st, "keys": nA, "new_keys": n_new, "keys_per_s": nA / sec,
                             "algorithmic_bytes": ibytes, "gbs": ibytes / sec / 1e9}
@@ -1051,6 +1181,18 @@ def main():
             "bytes_note": f"the block insert's {INSERT_BYTES_NEW}/{INSERT_BYTES_PRESENT} B per "
                           f"new/present key, {RADIX_INSERT_BYTES_RECORD} B per record (parent "
                           f"key), {RADIX_INSERT_BYTES_EDGE} B per edge walked",
+        }
+    if maint_cfg:
+        eg = float(np.mean([phases[W.MODE_NAMES[m]]["evict"]["gbs"] for m in modes]))
+        result["roofline_evict"] = {
+            "bound": "hbm", "kernel": "k_rank_hist/k_rank_select x 8 + k_compact + "
+                                      "k_rebuild_fill + k_reinsert (kvgov_cache_evict)",
+            "achieved": eg, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": eg / HBM_PEAK_GBS,
+            "traffic": None,
+            "bytes_note": f"{EVICT_BYTES_PER_SLOT} B per slot, {MAINT_BYTES_PER_KEPT} B per kept "
+                          "key (max_keys used as the kept count)",
+            "launch_ms": {W.MODE_NAMES[m]: phases[W.MODE_NAMES[m]]["evict"]["ms_median"]
+                          for m in modes},
         }
     if not probe_only and not admission and not radix_cfg:
         ins_gbs = float(np.mean([phases[W.MODE_NAMES[m]]["insert"]["gbs"] for m in modes]))
@@ -1144,7 +1286,8 @@ def main():
         if roof["bound"] == "alu":
             roof["frac_of_measured_peak"] = roof["achieved"] / mp["int_valu_tops"]
         for key in ("roofline_lookup", "roofline_insert", "roofline_admit",
-                    "roofline_radix_match", "roofline_radix_insert", "roofline"):
+                    "roofline_radix_match", "roofline_radix_insert", "roofline_evict",
+                    "roofline"):
             rr = result.get(key)
             if rr and rr["bound"] == "hbm":
                 rr["frac_of_measured_gather32"] = rr["achieved"] / mp["gather32_gbs"]

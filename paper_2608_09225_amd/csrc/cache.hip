@@ -378,15 +378,119 @@ struct SelectState {
   long long budget;              // keys still allowed below the decided part
   unsigned long long kept;       // keys copied out by the compaction
   unsigned long long erased;     // keys marked by erase
+  unsigned long long n_dense;    // recency words gathered for the select
+  unsigned long long lo, hi;     // their minimum and maximum
   int32_t level;                 // 8-bit digits decided
   int32_t done;
 };
 
 constexpr int kRankBins = 256;
+constexpr int kCompactItems = 16;  // slots per thread per block step
 
-// Histogram of the next digit of the ranks that match the decided prefix
-// (occupied slots and the all-0xFF key), per workgroup in LDS.
-__global__ __launch_bounds__(256) void k_rank_hist(TableView t, const SelectState *st,
+// Exclusive prefix of v over the workgroup (256 threads) and the total; one
+// global atomic on `counter` per call reserves the workgroup's range, whose
+// start is returned in *base.  Several hundred workgroups hitting one counter
+// once per 4096 slots cost little; once per wave they serialised (~200 us
+// for a 2^20-slot table).
+__device__ __forceinline__ uint32_t block_reserve(uint32_t v, unsigned long long *counter,
+                                                  unsigned long long *base) {
+  __shared__ uint32_t wsum[4];
+  __shared__ unsigned long long wbase;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  uint32_t inc = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t u = __shfl_up(inc, d, 64);
+    if (lane >= d) inc += u;
+  }
+  if (lane == 63) wsum[w] = inc;
+  __syncthreads();
+  uint32_t before = 0, total = 0;
+  for (int i = 0; i < 4; ++i) {
+    before += i < w ? wsum[i] : 0u;
+    total += wsum[i];
+  }
+  if (threadIdx.x == 0) wbase = total ? atomicAdd(counter, (unsigned long long)total) : 0ull;
+  __syncthreads();
+  *base = wbase;
+  __syncthreads();  // wsum and wbase are reused by the next call
+  return before + inc - v;
+}
+
+// Gathers the recency words of the occupied slots (and of the all-0xFF key)
+// into a dense array: the select passes then read 8 bytes per key instead
+// of 16 per slot.
+__global__ __launch_bounds__(256) void k_gather_ranks(TableView t, SelectState *st,
+                                                      unsigned long long *dense) {
+  const int64_t slots = (int64_t)t.mask + 1;
+  const int64_t step = (int64_t)256 * kCompactItems;
+  for (int64_t b0 = (int64_t)blockIdx.x * step; b0 < slots; b0 += (int64_t)gridDim.x * step) {
+    unsigned long long r[kCompactItems];
+    uint32_t have = 0;
+#pragma unroll
+    for (int k = 0; k < kCompactItems; ++k) {
+      const int64_t s = b0 + (int64_t)k * 256 + threadIdx.x;
+      r[k] = 0;
+      if (s < slots && t.tags[s] != 0) {
+        r[k] = t.rank[s];
+        have |= 1u << k;
+      }
+    }
+    unsigned long long base;
+    uint32_t at = block_reserve(__popc(have), &st->n_dense, &base);
+    unsigned long long mn = ~0ull, mx = 0;
+#pragma unroll
+    for (int k = 0; k < kCompactItems; ++k) {
+      if (have & (1u << k)) {
+        dense[base + at++] = r[k];
+        mn = r[k] < mn ? r[k] : mn;
+        mx = r[k] > mx ? r[k] : mx;
+      }
+    }
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+      const unsigned long long a = __shfl_xor(mn, d, 64), b = __shfl_xor(mx, d, 64);
+      mn = a < mn ? a : mn;
+      mx = b > mx ? b : mx;
+    }
+    if ((threadIdx.x & 63) == 0 && mx) {
+      atomicMin(&st->lo, mn);
+      atomicMax(&st->hi, mx);
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0 && t.meta->ones_present) {
+    const unsigned long long r = t.meta->ones_rank;
+    dense[atomicAdd(&st->n_dense, 1ull)] = r;
+    atomicMin(&st->lo, r);
+    atomicMax(&st->hi, r);
+  }
+}
+
+// Starts the select below the leading digits that all gathered words share
+// (typically the high bytes of the stamp and of the depth), or ends it when
+// they form one class.
+__global__ void k_select_start(SelectState *st) {
+  if (st->n_dense == 0) {
+    st->done = 1;
+    return;
+  }
+  const unsigned long long lo = st->lo, hi = st->hi;
+  if (lo == hi) {
+    st->threshold = st->n_dense <= (unsigned long long)st->budget ? 0ull : lo + 1;
+    st->done = 1;
+    return;
+  }
+  const int level = __builtin_clzll(lo ^ hi) / 8;  // 0..7
+  st->level = level;
+  st->prefix = level ? lo >> (64 - 8 * level) : 0ull;
+}
+
+// Histogram of the next digit of the gathered words that match the decided
+// prefix, per workgroup in LDS.  Most keys of a table share the leading
+// digits, so each wave first adds its lanes that share the first active
+// lane's bin with one atomic.
+__global__ __launch_bounds__(256) void k_rank_hist(const SelectState *st,
+                                                   const unsigned long long *dense,
                                                    unsigned int *hist) {
   __shared__ unsigned int h[kRankBins];
   if (st->done) return;
@@ -395,16 +499,27 @@ __global__ __launch_bounds__(256) void k_rank_hist(TableView t, const SelectStat
   const int level = st->level;
   const unsigned long long prefix = st->prefix;
   const int shift = 56 - 8 * level;
-  const int64_t slots = (int64_t)t.mask + 1;
-  for (int64_t s = (int64_t)blockIdx.x * 256 + threadIdx.x; s < slots;
-       s += (int64_t)gridDim.x * 256) {
-    if (t.tags[s] == 0) continue;
-    const uint64_t r = t.rank[s];
-    if (level == 0 || (r >> (shift + 8)) == prefix) atomicAdd(&h[(r >> shift) & 255], 1u);
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0 && t.meta->ones_present) {
-    const uint64_t r = t.meta->ones_rank;
-    if (level == 0 || (r >> (shift + 8)) == prefix) atomicAdd(&h[(r >> shift) & 255], 1u);
+  const int64_t n = (int64_t)st->n_dense;
+  const int lane = threadIdx.x & 63;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  // every lane of a wave runs the same number of rounds (ballot inside)
+  const int64_t rounds = (n + stride - 1) / stride;
+  for (int64_t k = 0; k < rounds; ++k) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x + k * stride;
+    bool valid = false;
+    int bin = 0;
+    if (i < n) {
+      const unsigned long long r = dense[i];
+      valid = level == 0 || (r >> (shift + 8)) == prefix;
+      bin = (int)((r >> shift) & 255);
+    }
+    const uint64_t act = __ballot(valid);
+    if (!act) continue;
+    const int leader = __builtin_ctzll(act);
+    const int lbin = __shfl(bin, leader, 64);
+    const uint64_t same = __ballot(valid && bin == lbin);
+    if (lane == leader) atomicAdd(&h[lbin], (unsigned int)__popcll(same));
+    if (valid && bin != lbin) atomicAdd(&h[bin], 1u);
   }
   __syncthreads();
   if (h[threadIdx.x]) atomicAdd(&hist[threadIdx.x], h[threadIdx.x]);
@@ -457,6 +572,9 @@ __global__ void k_select_init(SelectState *st, unsigned int *hist, long long bud
     st->budget = budget;
     st->kept = 0;
     st->erased = 0;
+    st->n_dense = 0;
+    st->lo = ~0ull;
+    st->hi = 0;
     st->level = 0;
     st->done = erase;
   }
@@ -479,48 +597,46 @@ __global__ __launch_bounds__(256) void k_erase_mark(TableView t, const uint8_t *
   if (w && atomicExch(w, kErased) != kErased) atomicAdd(&st->erased, 1ull);
 }
 
-// Copies the kept keys and their recency to scratch (one atomic per wave).
+// Copies the kept keys and their recency to scratch (one atomic per
+// workgroup step of 4096 slots).
 __global__ __launch_bounds__(256) void k_compact(TableView t, SelectState *st, u32x4 *out_keys,
                                                  unsigned long long *out_rank, int64_t cap) {
   const int64_t slots = (int64_t)t.mask + 1;
-  const int64_t stride = (int64_t)gridDim.x * 256;
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const unsigned long long thr = st->threshold;
-  const int lane = threadIdx.x & 63;
-  // every lane of a wave runs the same number of rounds (ballot inside);
-  // round -1 is the all-0xFF key, on lane 0 of the first wave
-  const int64_t rounds = (slots + stride - 1) / stride;
-  for (int64_t k = (gid < 64 ? -1 : 0); k < rounds; ++k) {
-    bool have = false;
-    unsigned long long r = 0;
-    u32x4 lo{}, hi{};
-    if (k < 0) {
-      r = t.meta->ones_rank;
-      have = gid == 0 && t.meta->ones_present && r != kErased && r >= thr;
-      lo = hi = u32x4{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
-    } else {
-      const int64_t s = gid + k * stride;
+  const int64_t step = (int64_t)256 * kCompactItems;
+  for (int64_t b0 = (int64_t)blockIdx.x * step; b0 < slots; b0 += (int64_t)gridDim.x * step) {
+    uint32_t keep = 0;
+#pragma unroll
+    for (int k = 0; k < kCompactItems; ++k) {
+      const int64_t s = b0 + (int64_t)k * 256 + threadIdx.x;
       if (s < slots && t.tags[s] != 0) {
-        r = t.rank[s];
-        if (r != kErased && r >= thr) {
-          have = true;
-          lo = t.keys[2 * s];
-          hi = t.keys[2 * s + 1];
-        }
+        const unsigned long long r = t.rank[s];
+        if (r != kErased && r >= thr) keep |= 1u << k;
       }
     }
-    const uint64_t mask = __ballot(have);
-    if (!mask) continue;
-    const int leader = __builtin_ctzll(mask);
-    unsigned long long base = 0;
-    if (lane == leader) base = atomicAdd(&st->kept, (unsigned long long)__popcll(mask));
-    base = __shfl(base, leader, 64);
-    if (have) {
-      const int64_t at = (int64_t)base + __popcll(mask & ((1ull << lane) - 1ull));
-      if (at < cap) {
-        out_keys[2 * at] = lo;
-        out_keys[2 * at + 1] = hi;
-        out_rank[at] = r;
+    unsigned long long base;
+    uint32_t at = block_reserve(__popc(keep), &st->kept, &base);
+#pragma unroll
+    for (int k = 0; k < kCompactItems; ++k) {
+      if (!(keep & (1u << k))) continue;
+      const int64_t s = b0 + (int64_t)k * 256 + threadIdx.x;
+      const int64_t o = (int64_t)(base + at++);
+      if (o < cap) {
+        out_keys[2 * o] = t.keys[2 * s];
+        out_keys[2 * o + 1] = t.keys[2 * s + 1];
+        out_rank[o] = t.rank[s];
+      }
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0 && t.meta->ones_present) {
+    const unsigned long long r = t.meta->ones_rank;
+    if (r != kErased && r >= thr) {
+      const int64_t o = (int64_t)atomicAdd(&st->kept, 1ull);
+      if (o < cap) {
+        const u32x4 ones = u32x4{0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu, 0xFFFFFFFFu};
+        out_keys[2 * o] = ones;
+        out_keys[2 * o + 1] = ones;
+        out_rank[o] = r;
       }
     }
   }
@@ -623,6 +739,13 @@ struct MaintScratch {
   int64_t cap = 0;
 };
 
+// Workgroups of the compaction kernels: one step of 4096 slots each, at most
+// 4 per CU.
+unsigned compact_grid(int64_t slots) {
+  return (unsigned)std::max<int64_t>(
+      1, std::min<int64_t>(ceil_div(slots, 256 * kCompactItems), (int64_t)device_cu_count() * 4));
+}
+
 int maint_alloc(kvgov_cache *c, hipStream_t s, MaintScratch &m) {
   m.cap = c->slots + 1;
   const size_t off_hist = 256;
@@ -646,7 +769,7 @@ int compact_rebuild(kvgov_cache *c, hipStream_t s, MaintScratch &m, const unsign
   const uint32_t epoch = c->epoch.fetch_add(1) + 1;
   int rc = epoch == 0xFFFFFFFFu ? KVGOV_E_UNSUPPORTED : KVGOV_OK;
   if (rc == KVGOV_OK) {
-    hipLaunchKernelGGL(k_compact, dim3(grid_for(c->slots, 32)), dim3(256), 0, s, c->view, m.st,
+    hipLaunchKernelGGL(k_compact, dim3(compact_grid(c->slots)), dim3(256), 0, s, c->view, m.st,
                        m.keys, m.rank, m.cap);
     hipLaunchKernelGGL(k_rebuild_fill, dim3(grid_for(c->slots, 64)), dim3(256), 0, s, c->view);
     hipLaunchKernelGGL(k_reinsert, dim3(grid_for(m.cap, 16)), dim3(256), 0, s, c->view, m.st,
@@ -878,9 +1001,15 @@ int kvgov_cache_evict(kvgov_cache *c, int64_t max_keys, int64_t *n_kept, void *s
   if (rc != KVGOV_OK) return rc;
   hipLaunchKernelGGL(k_select_init, dim3(1), dim3(kRankBins), 0, s, m.st, m.hist,
                      (long long)max_keys, 0);
+  // the gathered words live in the key area of the scratch until the
+  // compaction overwrites it
+  unsigned long long *dense = reinterpret_cast<unsigned long long *>(m.keys);
+  hipLaunchKernelGGL(k_gather_ranks, dim3(compact_grid(c->slots)), dim3(256), 0, s, c->view,
+                     m.st, dense);
+  hipLaunchKernelGGL(k_select_start, dim3(1), dim3(1), 0, s, m.st);
   for (int level = 0; level < 8; ++level) {
-    hipLaunchKernelGGL(k_rank_hist, dim3(grid_for(c->slots, 16)), dim3(256), 0, s, c->view,
-                       m.st, m.hist);
+    hipLaunchKernelGGL(k_rank_hist, dim3(grid_for(c->slots, 4)), dim3(256), 0, s, m.st, dense,
+                       m.hist);
     hipLaunchKernelGGL(k_rank_select, dim3(1), dim3(kRankBins), 0, s, m.st, m.hist);
   }
   return compact_rebuild(c, s, m, &m.st->kept, n_kept);

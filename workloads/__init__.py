@@ -383,6 +383,19 @@ def radix(seed: int = SEED, n: int = 4096, P: int = 64) -> Workload:
                     [ROOT, NONE], base.log2_slots, dict(base.notes))
 
 
+def maintenance(seed: int = SEED, n: int = 4096, P: int = 64) -> Workload:
+    """The paper-shaped batches on a table that tracks recency: the insert
+    batch, then the re-lookup batch, in two insert calls; an eviction down
+    to half of the keys present, an erase of the first tenth of the insert
+    batch's rows, then a lookup of the re-lookup batch."""
+    base = paper(seed=seed, n=n, P=P)
+    notes = dict(base.notes)
+    notes["evict_fraction"] = 0.5
+    notes["erase_fraction"] = 0.1
+    return Workload("maintenance", base.K, base.principal_ids, base.insert, base.lookup,
+                    [ROOT, BOUNDARY], base.log2_slots, notes)
+
+
 CONFIGS = {
     "tiny": tiny,
     "paper": paper,
@@ -392,6 +405,7 @@ CONFIGS = {
     "session": session,
     "admission": admission,
     "radix": radix,
+    "maintenance": maintenance,
 }
 
 
