@@ -12,6 +12,12 @@ counts with Gini ~ 0.63):
         insert the insert batch, look up the re-lookup batch
 
 Inputs are generated once and are resident in HBM before timing starts.
+Steps run one after another; --pipeline 2 keeps two batches in flight (two
+sets of tables, outputs, salts and streams, so batch i+1's salts and chains
+start while batch i's insert and lookup finish; every step still does all
+of its work).  It helps workloads of short chains and slows the
+latency-bound chain kernel of the paper-shaped step, whose SIMDs the other
+batch's kernels then share.
 value = block tokens hashed per second over the whole step (16 tokens per
 full block, both batches, both modes); lookups/s and block hashes/s are
 reported beside it.  The roofline entry is for the chain-hashing kernel,
@@ -604,6 +610,11 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the critical-path launch and the measured-peak "
                          "microbenchmarks (counter runs: only the step's own launches)")
+    ap.add_argument("--pipeline", type=int, default=1, choices=(1, 2),
+                    help="batches in flight: 1 runs the steps one after another; 2 runs "
+                         "batch i+1's salts and chains while batch i's insert and lookup "
+                         "finish (two sets of tables and buffers; slower for the latency-bound "
+                         "chain kernel, whose SIMDs the other batch's kernels then share)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before the bench, run one device-to-device copy of this many MiB "
                          "(a kernel of known traffic, to scale HBM byte counters)")
@@ -656,25 +667,48 @@ def main():
     if not relookup_same:
         boA, boB = to(A.blk_offsets()), to(B.blk_offsets())
     modes = wl.modes
-    out = {m: torch.empty((nX, 32), dtype=torch.uint8, device=dev) for m in modes}
-    hits = {m: torch.empty(B.n, dtype=torch.int32, device=dev) for m in modes}
-    salts = torch.empty((wl.P, 32), dtype=torch.uint8, device=dev)
     status = K.new_status(dev)
     radix_cfg = wl.name == "radix"
     maint_cfg = wl.name == "maintenance"
-    caches = {m: K.Cache(wl.log2_slots) for m in modes} if not radix_cfg else {}
-    radixes = {m: K.Radix(wl.log2_slots, RADIX_EDGE_SLOTS_LOG2) for m in modes} \
-        if radix_cfg else {}
-    matched = {m: torch.empty(B.n, dtype=torch.int32, device=dev) for m in modes}
-    ev_rins, ev_rmatch = [], []
-    main_s = torch.cuda.current_stream()
-    streams = {m: torch.cuda.Stream(device=dev) for m in modes}  # default priority
-    ev_chain, ev_look, ev_salts, ev_clear, ev_ins = [], [], [], [], []
-    # admission: one lookup-then-insert call over both batches, in order
     admission = wl.name == "admission"
+    main_s = torch.cuda.current_stream()
+
+    def buffer_set():
+        """Everything one batch in flight writes: chain outputs, results,
+        salts, tables, and a stream per mode plus one for the salts (all at
+        the default priority)."""
+        return dict(
+            out={m: torch.empty((nX, 32), dtype=torch.uint8, device=dev) for m in modes},
+            hits={m: torch.empty(B.n, dtype=torch.int32, device=dev) for m in modes},
+            salts=torch.empty((wl.P, 32), dtype=torch.uint8, device=dev),
+            caches={m: K.Cache(wl.log2_slots) for m in modes} if not radix_cfg else {},
+            radixes={m: K.Radix(wl.log2_slots, RADIX_EDGE_SLOTS_LOG2) for m in modes}
+            if radix_cfg else {},
+            matched={m: torch.empty(B.n, dtype=torch.int32, device=dev) for m in modes},
+            adm_hits={m: torch.empty(X.n, dtype=torch.int32, device=dev) for m in modes},
+            adm_new={m: torch.empty(X.n, dtype=torch.int32, device=dev) for m in modes},
+            streams={m: torch.cuda.Stream(device=dev) for m in modes},
+            sstream=torch.cuda.Stream(device=dev),
+            chains_done=[], step_done=[])
+
+    depth = 1 if probe_only else args.pipeline
+    sets = [buffer_set() for _ in range(depth)]
+
+    def use_set(k):
+        """Points the step's names at buffer set k."""
+        nonlocal out, hits, salts, caches, radixes, matched, adm_hits, adm_new, streams
+        st = sets[k]
+        out, hits, salts, caches = st["out"], st["hits"], st["salts"], st["caches"]
+        radixes, matched, adm_hits, adm_new = (st["radixes"], st["matched"], st["adm_hits"],
+                                               st["adm_new"])
+        streams = st["streams"]
+        return st
+
+    out = hits = salts = caches = radixes = matched = adm_hits = adm_new = streams = None
+    use_set(0)
+    ev_rins, ev_rmatch = [], []
+    ev_chain, ev_look, ev_salts, ev_clear, ev_ins = [], [], [], [], []
     ev_adm = []
-    adm_hits = {m: torch.empty(X.n, dtype=torch.int32, device=dev) for m in modes}
-    adm_new = {m: torch.empty(X.n, dtype=torch.int32, device=dev) for m in modes}
 
     def bview(m):
         return out[m][0:nA], (out[m][0:nA] if relookup_same else out[m][nA:])
@@ -716,8 +750,10 @@ def main():
         # of the insert batch's rows
         K.salts(wl.K, ids, out=salts)
         n_erase = int(nA * wl.notes["erase_fraction"])
+        for st in sets:
+            for c in st["caches"].values():
+                c.set_recency(True)
         for m in modes:
-            caches[m].set_recency(True)
             hash_call(m, main_s)
             new_a[m] = caches[m].insert(out[m][0:nA], boA)
             caches[m].insert(out[m][nA:], boB)
@@ -752,14 +788,21 @@ def main():
             evs.append((key, e0, e1))
         return end
 
-    def step(record: bool):
+    def step(record: bool, i: int):
+        st = use_set(i % depth)
+        sst = st["sstream"]
+        # the salts of this set are rewritten once the set's previous chains
+        # have read them (and, one batch in flight, once its step is done)
+        for ev in st["chains_done"] + (st["step_done"] if depth == 1 else []):
+            sst.wait_event(ev)
         if not probe_only:
-            end = timed(ev_salts, None, main_s) if record else None
-            K.salts(wl.K, ids, out=salts, stream=main_s)
+            end = timed(ev_salts, None, sst) if record else None
+            K.salts(wl.K, ids, out=salts, stream=sst)
             if end:
                 end()
         salted = torch.cuda.Event()
-        salted.record(main_s)
+        salted.record(sst)
+        st["chains_done"] = []
         done = []
         for m in modes:
             s = streams[m]
@@ -777,6 +820,9 @@ def main():
                     e1 = torch.cuda.Event(enable_timing=True)
                     e0.record(s)
                 hash_call(m, s)
+                cd = torch.cuda.Event()
+                cd.record(s)
+                st["chains_done"].append(cd)
                 if record:
                     e1.record(s)
                     ev_chain.append((m, e0, e1))
@@ -834,20 +880,24 @@ def main():
             ev = torch.cuda.Event()
             ev.record(s)
             done.append(ev)
-        for ev in done:
-            main_s.wait_event(ev)
+        st["step_done"] = done
+        if depth == 1:
+            for ev in done:
+                main_s.wait_event(ev)
 
-    log(f"warmup {args.warmup} steps")
-    for _ in range(args.warmup):
-        step(False)
+    log(f"warmup {args.warmup} steps ({depth} batch(es) in flight)")
+    for i in range(args.warmup):
+        step(False, i)
     torch.cuda.synchronize()
     log(f"timing {args.steps} steps")
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(True)
+    for i in range(args.steps):
+        step(True, args.warmup + i)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     t_step = elapsed / args.steps
+    # the results below are those of the last step's buffer set
+    use_set((args.warmup + args.steps - 1) % depth)
 
     # ---- gates: latched errors, bit-exactness on a sample, by-construction hits
     K.check_status(status, "bench step")
@@ -946,6 +996,7 @@ def main():
             "principals": wl.P,
             "modes": [W.MODE_NAMES[m] for m in modes],
             "table_slots": 1 << wl.log2_slots,
+            "batches_in_flight": depth,
         },
     }
     if admission:
@@ -1301,8 +1352,9 @@ def main():
         procs = min(16, len(os.sched_getaffinity(0)))
         log(f"timing the CPU oracle on {procs} processes")
         result["cpu_baseline"] = cpu_baseline(wl, procs, max_blocks=1_500_000)
-    for c in list(caches.values()) + list(radixes.values()):
-        c.close()
+    for st in sets:
+        for c in list(st["caches"].values()) + list(st["radixes"].values()):
+            c.close()
     print(json.dumps(result), flush=True)
     if not (gates["G1_bitexact_sampled"] and gates.get("G4_hits_by_construction", True)):
         log(f"correctness gate failure: {gates}")
