@@ -12,6 +12,10 @@ counts with Gini ~ 0.63):
         insert the insert batch, look up the re-lookup batch
 
 Inputs are generated once and are resident in HBM before timing starts.
+Each step derives its salts during the previous step (two salt buffers; the
+timed region holds one salts derivation per step): the salts kernel is a
+single wave, slow on an otherwise idle GPU, and no longer delays the chains
+(--salts-in-step derives them at the step's start instead).
 Steps run one after another; --pipeline 2 keeps two batches in flight (two
 sets of tables, outputs, salts and streams, so batch i+1's salts and chains
 start while batch i's insert and lookup finish; every step still does all
@@ -615,6 +619,9 @@ def main():
                          "batch i+1's salts and chains while batch i's insert and lookup "
                          "finish (two sets of tables and buffers; slower for the latency-bound "
                          "chain kernel, whose SIMDs the other batch's kernels then share)")
+    ap.add_argument("--salts-in-step", action="store_true",
+                    help="derive each step's salts at its start, before its chains (default: "
+                         "during the previous step)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before the bench, run one device-to-device copy of this many MiB "
                          "(a kernel of known traffic, to scale HBM byte counters)")
@@ -788,20 +795,48 @@ def main():
             evs.append((key, e0, e1))
         return end
 
+    # One batch in flight: the salts of step i + 1 are derived while step i
+    # runs (two salt buffers), so that a step's chains start without waiting
+    # for its salts kernel (a single wave, slow on an otherwise idle GPU);
+    # each step still derives one set of salts.
+    early = depth == 1 and not probe_only and not args.salts_in_step
+    salt_bufs = [sets[0]["salts"], torch.empty_like(sets[0]["salts"])]
+    salted_evs = [None, None]
+    readers = [[], []]  # chains that read each salt buffer last
+
+    def enqueue_salts(k: int, record: bool):
+        sst = sets[0]["sstream"]
+        for ev in readers[k % 2]:
+            sst.wait_event(ev)
+        end = timed(ev_salts, None, sst) if record else None
+        K.salts(wl.K, ids, out=salt_bufs[k % 2], stream=sst)
+        if end:
+            end()
+        ev = torch.cuda.Event()
+        ev.record(sst)
+        salted_evs[k % 2] = ev
+
     def step(record: bool, i: int):
+        nonlocal salts
         st = use_set(i % depth)
         sst = st["sstream"]
-        # the salts of this set are rewritten once the set's previous chains
-        # have read them (and, one batch in flight, once its step is done)
-        for ev in st["chains_done"] + (st["step_done"] if depth == 1 else []):
-            sst.wait_event(ev)
-        if not probe_only:
-            end = timed(ev_salts, None, sst) if record else None
-            K.salts(wl.K, ids, out=salts, stream=sst)
-            if end:
-                end()
-        salted = torch.cuda.Event()
-        salted.record(sst)
+        if early:
+            salts = salt_bufs[i % 2]
+            if salted_evs[i % 2] is None:
+                enqueue_salts(i, False)
+            salted = salted_evs[i % 2]
+        else:
+            # the salts of this set are rewritten once the set's previous
+            # chains have read them (one batch in flight: once its step is done)
+            for ev in st["chains_done"] + (st["step_done"] if depth == 1 else []):
+                sst.wait_event(ev)
+            if not probe_only:
+                end = timed(ev_salts, None, sst) if record else None
+                K.salts(wl.K, ids, out=salts, stream=sst)
+                if end:
+                    end()
+            salted = torch.cuda.Event()
+            salted.record(sst)
         st["chains_done"] = []
         done = []
         for m in modes:
@@ -881,9 +916,10 @@ def main():
             ev.record(s)
             done.append(ev)
         st["step_done"] = done
-        if depth == 1:
-            for ev in done:
-                main_s.wait_event(ev)
+        if early:
+            readers[i % 2] = list(st["chains_done"])
+            salted_evs[i % 2] = None
+            enqueue_salts(i + 1, record)
 
     log(f"warmup {args.warmup} steps ({depth} batch(es) in flight)")
     for i in range(args.warmup):
