@@ -1164,7 +1164,16 @@ def main():
         }
         result["roofline_admit" if admission else
                "roofline_radix_match" if radix_cfg else "roofline_lookup"] = roof_lookup
-        per_step = [sum(chain_t[m][i] for m in modes) for i in range(args.steps)]
+        # per step: from the first chain launch's start to the last one's end
+        # (the modes' launches overlap, and how they share the chip shifts
+        # between steps, so the sum of their durations is the noisier figure)
+        nm = len(modes)
+        per_step = []
+        for i in range(args.steps):
+            evs = ev_chain[i * nm:(i + 1) * nm]
+            ref = evs[0][1]
+            per_step.append(max(ref.elapsed_time(e1) for _, _, e1 in evs) * 1e-3 -
+                            min(ref.elapsed_time(e0) for _, e0, _ in evs) * 1e-3)
         if wl.name == "template":
             s = {W.MODE_NAMES[m]: int(got_hits[m].sum()) for m in modes}
             result["hit_blocks"] = s

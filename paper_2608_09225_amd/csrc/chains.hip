@@ -47,6 +47,9 @@
 #ifndef KVGOV_LP_COVER
 #define KVGOV_LP_COVER 2  // lane-pair kernel: steps between a barrier and its first word
 #endif
+#ifndef KVGOV_LP_GROUPS
+#define KVGOV_LP_GROUPS 16, 32, 48, 64  // lane-pair kernel: schedule group bounds
+#endif
 
 namespace kvgov {
 
@@ -801,6 +804,103 @@ __device__ __forceinline__ void lp_sched16(uint32_t w[16], uint32_t (*rows)[kLpC
   }
 }
 
+// schedule words W[T0..T0+N-1] (T0 >= 16) from the rolling window w, which
+// holds W[t] at w[t & 15]; stores K[t] + W[t] to rows[t - 16][lane].  With
+// PRE, the terms of W[16..30] that depend on message words 8..15 alone come
+// from pre (lp_presum), computed while the previous block was hashed.
+template <int T0, int N, bool PRE>
+__device__ __forceinline__ void lp_sched_words(uint32_t w[16], uint32_t (*rows)[kLpCols],
+                                               int lane, const uint32_t pre[16]) {
+#pragma unroll
+  for (int t = T0; t < T0 + N; ++t) {
+    uint32_t v;
+    if (PRE && (t == 16 || t == 17))
+      v = small_sigma0(w[(t - 15) & 15]) + w[t & 15] + pre[t - 16];
+    else if (PRE && t == 23)
+      v = small_sigma1(w[(t - 2) & 15]) + w[(t - 7) & 15] + pre[7] + w[t & 15];
+    else if (PRE && t >= 24 && t <= 30)
+      v = small_sigma1(w[(t - 2) & 15]) + w[(t - 7) & 15] + pre[t - 16];
+    else
+      v = small_sigma1(w[(t - 2) & 15]) + w[(t - 7) & 15] + small_sigma0(w[(t - 15) & 15]) +
+          w[t & 15];
+    w[t & 15] = v;
+    rows[t - 16][lane] = v + kSha.K[t];
+  }
+}
+
+// The parts of schedule words 16..30 of a first compression whose message
+// words 8..15 are m[0..7] (every block but the chain's first and the
+// boundary block) that do not involve words 0..7:
+//   W16 = sigma0(W1) + W0 + [sigma1(W14) + W9]     W17 likewise
+//   W23 = sigma1(W21) + W16 + W7 + [sigma0(W8)]
+//   W24..W30 = sigma1(W[t-2]) + W[t-7] + [sigma0(W[t-15]) + W[t-16]]
+__device__ __forceinline__ void lp_presum(const uint32_t m[8], uint32_t pre[16]) {
+  pre[0] = small_sigma1(m[6]) + m[1];
+  pre[1] = small_sigma1(m[7]) + m[2];
+  pre[7] = small_sigma0(m[0]);
+#pragma unroll
+  for (int i = 0; i < 7; ++i) pre[8 + i] = small_sigma0(m[1 + i]) + m[i];
+}
+
+// The first compression's schedule words W[16..63] depend on h_{j-1} and are
+// released to the rounds waves in groups, one barrier each: group g holds
+// W[kLpGroup[g] .. kLpGroup[g + 1] - 1].  The schedule wave produces a word
+// a little slower than the rounds consume one, so the groups shrink towards
+// the end of the compression: each group is complete by the time the rounds
+// reach its first word.
+constexpr int kLpGroup[] = {KVGOV_LP_GROUPS};
+constexpr int kLpGroups = (int)(sizeof(kLpGroup) / sizeof(kLpGroup[0])) - 1;
+static_assert(kLpGroup[0] == 16 && kLpGroup[kLpGroups] == 64, "groups cover W[16..63]");
+
+template <int G>
+__device__ __forceinline__ void lp_sched_groups(uint32_t w[16], uint32_t (*rows)[kLpCols],
+                                                int lane, bool work, const uint32_t pre[16],
+                                                bool use_pre) {
+  if constexpr (G < kLpGroups) {
+    constexpr int S = kLpGroup[G], N = kLpGroup[G + 1] - kLpGroup[G];
+    static_assert(N > 0, "groups ascend");
+    if (work) {
+      if (S <= 30 && use_pre)  // workgroup-uniform
+        lp_sched_words<S, N, true>(w, rows, lane, pre);
+      else
+        lp_sched_words<S, N, false>(w, rows, lane, pre);
+    }
+    __syncthreads();
+    lp_sched_groups<G + 1>(w, rows, lane, work, pre, use_pre);
+  }
+}
+
+// Rounds of the first compression from step kLpGroup[G] - C on: after the
+// barrier that releases group G, its K + W rows are loaded into kw and the
+// steps up to the next group's barrier (or to step 63) run.  kw2 receives
+// the second compression's first 16 K + W rows during the last group.
+template <int G>
+__device__ __forceinline__ void lp_round_groups(uint32_t s[4], uint32_t &z, uint32_t kw[64],
+                                                uint32_t kw2[16],
+                                                const uint32_t (*rows)[kLpCols],
+                                                const uint32_t (*rows2)[kLpCols], int col,
+                                                const LpLane &c, bool act) {
+  if constexpr (G < kLpGroups) {
+    constexpr int C = KVGOV_LP_COVER;
+    constexpr int S = kLpGroup[G], E = kLpGroup[G + 1];
+    __syncthreads();  // releases W[S..E-1]
+    if (act) {
+#pragma unroll
+      for (int t = S; t < E; ++t) kw[t] = rows[t - 16][col];
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (E < 64) {
+        lp_steps<E - S>(s, z, kw + S - C, kw[E - C], c);
+      } else {
+        lp_steps<C>(s, z, kw + S - C, kw[S], c);
+        lp_load16(kw2, rows2, 0, col);
+        __builtin_amdgcn_sched_barrier(0);
+        lp_steps<64 - S>(s, z, kw + S, 1u, c);
+      }
+    }
+    lp_round_groups<G + 1>(s, z, kw, kw2, rows, rows2, col, c, act);
+  }
+}
+
 // Per block and request, the three message patterns of the chain (the
 // compressions of a block, "first" and "second", plus a third for the
 // boundary block):
@@ -962,6 +1062,9 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
   }
   __syncthreads();
 
+  uint32_t pre[16];  // schedule lanes: partial sums of the next block's first schedule
+#pragma unroll
+  for (int x = 0; x < 16; ++x) pre[x] = 0;
   for (int64_t j = 0; j < J; ++j) {
     const bool act = j < nf;
     const bool next = j + 1 < nf;
@@ -979,43 +1082,24 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
       // first word it releases is taken, so that the LDS reads after it are
       // covered by those steps.
       constexpr int C = KVGOV_LP_COVER;
-      uint32_t s[4], st[4], wa[16], wb[16], z = 0;
-      uint32_t kw16[16];
+      uint32_t s[4], st[4], wa[16], z = 0;
+      uint32_t kw[64];
       if (act) {
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-          kw16[t] = kSha.K[t] + L.ha[t][col];
-          kw16[8 + t] = kSha.K[8 + t] + L.hb[t][col];
+          kw[t] = kSha.K[t] + L.ha[t][col];
+          kw[8 + t] = kSha.K[8 + t] + L.hb[t][col];
         }
 #pragma unroll
         for (int x = 0; x < 4; ++x) s[x] = a_lane ? (x < 2 ? iv[x + 2] : 0u) : iv[x];
-        z = lp_z0(s, kw16[0], c);
-        lp_head(s, z, kw16[1], kw16[2], c, iv[1], iv[0], a_lane);
-        lp_steps<6>(s, z, kw16 + 2, kw16[8], c);  // steps 2..7
-        lp_steps<8 - C>(s, z, kw16 + 8, kw16[16 - C], c);
+        z = lp_z0(s, kw[0], c);
+        lp_head(s, z, kw[1], kw[2], c, iv[1], iv[0], a_lane);
+        lp_steps<6>(s, z, kw + 2, kw[8], c);  // steps 2..7
+        lp_steps<8 - C>(s, z, kw + 8, kw[16 - C], c);
       }
-      __syncthreads();  // first compression, rounds 16..31 ready
+      // steps 16 - C .. 63, one barrier per schedule group
+      lp_round_groups<0>(s, z, kw, wa, L.c1b, L.c2[cb], col, c, act);
       if (act) {
-        lp_load16(wb, L.c1b, 0, col);
-        __builtin_amdgcn_sched_barrier(0);
-        lp_steps<C>(s, z, kw16 + 16 - C, wb[0], c);
-        lp_steps<16 - C>(s, z, wb, wb[16 - C], c);  // from 16
-      }
-      __syncthreads();  // rounds 32..47 ready
-      if (act) {
-        lp_load16(wa, L.c1b, 16, col);
-        __builtin_amdgcn_sched_barrier(0);
-        lp_steps<C>(s, z, wb + 16 - C, wa[0], c);
-        lp_steps<16 - C>(s, z, wa, wa[16 - C], c);  // from 32
-      }
-      __syncthreads();  // rounds 48..63 ready
-      if (act) {
-        lp_load16(wb, L.c1b, 32, col);
-        __builtin_amdgcn_sched_barrier(0);
-        lp_steps<C>(s, z, wa + 16 - C, wb[0], c);
-        lp_load16(wa, L.c2[cb], 0, col);
-        __builtin_amdgcn_sched_barrier(0);
-        lp_steps<16>(s, z, wb, 1u, c);  // 48..63
         lp_tail(s, z, c, a_lane);
 #pragma unroll
         for (int x = 0; x < 4; ++x) st[x] = iv[x] + s[x];
@@ -1052,13 +1136,10 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
           w[x] = L.ha[x][lane];
           w[8 + x] = L.hb[x][lane];
         }
-        lp_sched16<16>(w, L.c1b, 0, lane);
       }
-      __syncthreads();
-      if (act && !idle) lp_sched16<32>(w, L.c1b, 16, lane);
-      __syncthreads();
-      if (act && !idle) lp_sched16<48>(w, L.c1b, 32, lane);
-      __syncthreads();
+      // the partial sums hold for block j unless it is a chain's first
+      // block or some request's boundary block
+      lp_sched_groups<0>(w, L.c1b, lane, act && !idle, pre, j > 0 && !third);
       if (!idle) {
         // block j + 1's tokens, and the load of block j + 2
         uint32_t Tn[16];
@@ -1067,6 +1148,7 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
         if (next) {
           const bool bnd_next = MODE == KVGOV_BOUNDARY && j + 1 == kb;
           lp_prepare(Tn, q.sig, false, bnd_next, L, nb, lane);
+          lp_presum(Tn, pre);
         }
       }
       __syncthreads();
