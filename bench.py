@@ -1164,16 +1164,15 @@ def main():
         }
         result["roofline_admit" if admission else
                "roofline_radix_match" if radix_cfg else "roofline_lookup"] = roof_lookup
-        # per step: from the first chain launch's start to the last one's end
-        # (the modes' launches overlap, and how they share the chip shifts
-        # between steps, so the sum of their durations is the noisier figure)
+        # per step: the interval between consecutive steps' last chain ends
+        # (the steady-state step time; the modes' launches overlap and how
+        # they share the chip shifts between steps, so their durations are
+        # the noisier figure)
         nm = len(modes)
-        per_step = []
-        for i in range(args.steps):
-            evs = ev_chain[i * nm:(i + 1) * nm]
-            ref = evs[0][1]
-            per_step.append(max(ref.elapsed_time(e1) for _, _, e1 in evs) * 1e-3 -
-                            min(ref.elapsed_time(e0) for _, e0, _ in evs) * 1e-3)
+        ref = ev_chain[0][1]
+        ends = [max(ref.elapsed_time(e1) for _, _, e1 in ev_chain[i * nm:(i + 1) * nm]) * 1e-3
+                for i in range(args.steps)]
+        per_step = [b - a for a, b in zip(ends, ends[1:])]
         if wl.name == "template":
             s = {W.MODE_NAMES[m]: int(got_hits[m].sum()) for m in modes}
             result["hit_blocks"] = s
@@ -1388,9 +1387,12 @@ def main():
             if rr and rr["bound"] == "hbm":
                 rr["frac_of_measured_gather32"] = rr["achieved"] / mp["gather32_gbs"]
 
-    h = args.steps // 2
-    a1, a2 = np.mean(per_step[:h]), np.mean(per_step[h:])
-    gates["G3_two_halves_within_5pct"] = bool(abs(a1 - a2) / max(a1, a2) < 0.05)
+    # medians, so that one disturbed step does not decide the gate
+    h = len(per_step) // 2
+    if h:
+        a1, a2 = np.median(per_step[:h]), np.median(per_step[h:])
+        gates["G3_two_halves_within_5pct"] = bool(abs(a1 - a2) / max(a1, a2) < 0.05)
+    result["gate_steps_ms"] = [round(float(v) * 1e3, 4) for v in per_step]
     gates["G2_below_peak"] = bool(result["roofline"]["frac"] <= 1.0 and roof_lookup["frac"] <= 1.0)
     result["gates"] = gates
     if not args.no_cpu_baseline:
