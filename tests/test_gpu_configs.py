@@ -14,7 +14,14 @@ uses (one hashing call per batch and mode, the table sizes of the configs).
 * session (4096 two-turn sessions): turn 2's chains resumed from turn 1's
   last digests, every digest, n_new and hit count against the oracle's own
   resumed chains.
+* admission, radix, maintenance (the paper-shaped batches on the three
+  later stages, one call shape each as bench.py times them): every admitted
+  request's hits and new blocks against the oracle's sequential admission;
+  sampled token-granular matches against the oracle's index and every match
+  against the shared prefix; the maintained table (two tracked inserts, an
+  eviction to half, an erase, a re-lookup) replayed by the oracle.
 """
+import hashlib
 import os
 
 import numpy as np
@@ -249,3 +256,131 @@ def test_session_config(session_wl, mode):
     assert n_new == O.Table().insert(want) == int(cnt.sum())
     assert np.array_equal(hits, cnt)
     assert np.array_equal(hits, wl.lookup.expect_hits[mode])
+
+
+# ---------------------------------------------------------------------------
+# the later stages on the paper-shaped batches
+# ---------------------------------------------------------------------------
+
+_CHAINS = {}
+
+
+def oracle_chains_cached(b, salts, mode):
+    """The oracle's digests of a whole batch, computed once per content (the
+    three workloads below share the paper-shaped batches)."""
+    h = hashlib.sha256()
+    for a in (b.tokens, b.tok_offsets, b.principal, b.boundary_tok):
+        h.update(np.ascontiguousarray(a).tobytes())
+    h.update(b"".join(salts))
+    key = (h.hexdigest(), mode)
+    if key not in _CHAINS:
+        _CHAINS[key] = oracle_chains(b, salts, mode)
+    return _CHAINS[key]
+
+
+def concat(A, B):
+    return W.Batch(np.concatenate([A.tokens, B.tokens]),
+                   np.concatenate([A.tok_offsets, B.tok_offsets[1:] + A.tok_offsets[-1]]),
+                   np.concatenate([A.principal, B.principal]),
+                   np.concatenate([A.boundary_tok, B.boundary_tok]))
+
+
+@pytest.fixture(scope="module")
+def admission_wl():
+    return W.make("admission")
+
+
+@pytest.mark.parametrize("mode", [W.ROOT, W.BOUNDARY])
+def test_admission_config(admission_wl, mode):
+    """Both batches (8192 requests) admitted in one call, as bench.py does:
+    every request's hit blocks and new blocks against the oracle's requests
+    taken in order, and the hits fixed by construction."""
+    wl = admission_wl
+    A, B = wl.insert, wl.lookup
+    X = concat(A, B)
+    sd = K.salts(wl.K, dev(wl.principal_ids))
+    osalts = O.salts(wl.K, wl.principal_ids)
+    h = gpu_chains(X, sd, mode)
+    with K.Cache(wl.log2_slots) as c:
+        hits, new, n_new = c.admit(h, dev(X.blk_offsets()))
+        count = c.count()
+    want_h = np.concatenate([oracle_chains_cached(A, osalts, mode),
+                             oracle_chains_cached(B, osalts, mode)])
+    assert np.array_equal(h.cpu().numpy(), want_h)
+    T = O.Table()
+    wh, wn = T.admit(want_h, X.blk_offsets())
+    assert np.array_equal(hits.cpu().numpy(), wh)
+    assert np.array_equal(new.cpu().numpy(), wn)
+    assert n_new == int(wn.sum()) == len(T.keys) == count
+    assert np.array_equal(wh, wl.notes["admit_hits"][mode])
+
+
+@pytest.fixture(scope="module")
+def radix_wl():
+    return W.make("radix")
+
+
+@pytest.mark.parametrize("mode", [W.ROOT, W.NONE])
+def test_radix_config(radix_wl, mode):
+    """The insert batch's sequences into the radix index (2^23 edge slots, as
+    bench.py), the re-lookup batch matched: every match covers the shared
+    2119-token prefix, 96 sampled matches equal the oracle's, and the index
+    holds one block node per distinct digest plus its roots."""
+    wl = radix_wl
+    A, B = wl.insert, wl.lookup
+    sd = K.salts(wl.K, dev(wl.principal_ids))
+    osalts = O.salts(wl.K, wl.principal_ids)
+    salted = mode != W.NONE
+
+    def args(b):
+        h = gpu_chains(b, sd, mode) if salted else \
+            K.hash_chains(dev(b.tokens), dev(b.tok_offsets), None, None, W.NONE)
+        return (dev(b.tokens), dev(b.tok_offsets), dev(b.principal) if salted else None,
+                sd if salted else None, mode, h, dev(b.blk_offsets()))
+
+    with K.Radix(wl.log2_slots, 23) as x:
+        x.insert(*args(A))
+        got = x.match(*args(B)).cpu().numpy()
+        blocks, edges = x.stats()
+    assert (got >= wl.notes["prefix_len"]).all()
+    ha = oracle_chains_cached(A, osalts, mode)
+    roots = wl.P if salted else 1  # a root per salt of the table, or the zero root
+    assert blocks == roots + len({ha[i].tobytes() for i in range(ha.shape[0])})
+    qs = np.sort(np.random.default_rng(17).choice(B.n, 96, replace=False))
+    R = O.Radix()
+    R.insert(A.tokens, A.tok_offsets, A.principal, osalts, mode)
+    want = R.match(B.tokens, B.tok_offsets, B.principal, osalts, mode, requests=qs)
+    assert np.array_equal(got[qs], want)
+
+
+@pytest.fixture(scope="module")
+def maintenance_wl():
+    return W.make("maintenance")
+
+
+@pytest.mark.parametrize("mode", [W.ROOT, W.BOUNDARY])
+def test_maintenance_config(maintenance_wl, mode):
+    """A recency-tracking table: the insert batch and the re-lookup batch in
+    two insert calls, an eviction to half of the keys present, an erase of
+    the first tenth of the insert batch's rows, a lookup of the re-lookup
+    batch; every count, the kept key set and every hit against the oracle."""
+    wl = maintenance_wl
+    A, B = wl.insert, wl.lookup
+    sd = K.salts(wl.K, dev(wl.principal_ids))
+    osalts = O.salts(wl.K, wl.principal_ids)
+    hA, hB = gpu_chains(A, sd, mode), gpu_chains(B, sd, mode)
+    oA, oB = oracle_chains_cached(A, osalts, mode), oracle_chains_cached(B, osalts, mode)
+    n_erase = int(A.block_counts().sum() * wl.notes["erase_fraction"])
+    T = O.Table()
+    with K.Cache(wl.log2_slots) as c:
+        c.set_recency(True)
+        assert c.insert(hA, dev(A.blk_offsets())) == T.insert(oA, A.blk_offsets())
+        assert c.insert(hB, dev(B.blk_offsets())) == T.insert(oB, B.blk_offsets())
+        max_keys = int(c.count() * wl.notes["evict_fraction"])
+        assert c.evict(max_keys) == T.evict(max_keys)
+        assert c.erase(hA[:n_erase]) == T.erase(oA[:n_erase])
+        hits = c.lookup(hB, dev(B.blk_offsets())).cpu().numpy()
+        assert c.count() == len(T.keys)
+        kept = c.export().cpu().numpy()
+    assert {kept[i].tobytes() for i in range(kept.shape[0])} == T.keys
+    assert np.array_equal(hits, T.lookup(oB, B.blk_offsets()))
