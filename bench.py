@@ -629,8 +629,8 @@ def main():
                          "(a kernel of known traffic, to scale HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
-                                   "(multi-GPU sharding is a design note, not built)"}))
+        print(json.dumps({"error": "the bench runs on one GPU only; --gpus must be 1 "
+                                   "(sharding over several GPUs is not implemented)"}))
         sys.exit(2)
 
     import torch
