@@ -844,10 +844,10 @@ __device__ __forceinline__ void lp_presum(const uint32_t m[8], uint32_t pre[16])
 
 // The first compression's schedule words W[16..63] depend on h_{j-1} and are
 // released to the rounds waves in groups, one barrier each: group g holds
-// W[kLpGroup[g] .. kLpGroup[g + 1] - 1].  The schedule wave produces a word
-// a little slower than the rounds consume one, so the groups shrink towards
-// the end of the compression: each group is complete by the time the rounds
-// reach its first word.
+// W[kLpGroup[g] .. kLpGroup[g + 1] - 1].  A barrier costs the waves about as
+// much as the rounds lose waiting for a larger group (the schedule wave
+// makes a word a little slower than the rounds use one): three groups of 16
+// measured fastest, splits into 4 to 8 groups slower.
 constexpr int kLpGroup[] = {KVGOV_LP_GROUPS};
 constexpr int kLpGroups = (int)(sizeof(kLpGroup) / sizeof(kLpGroup[0])) - 1;
 static_assert(kLpGroup[0] == 16 && kLpGroup[kLpGroups] == 64, "groups cover W[16..63]");
