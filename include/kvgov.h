@@ -197,7 +197,8 @@ int kvgov_resume_offsets(const int64_t *tok_offsets, const int32_t *start_block,
  * slots of 32-byte keys with full 256-bit compare; any 32-byte value is a
  * valid key.  No eviction: a key stays until kvgov_cache_clear.
  *
- * create: allocates about 36 * 2^log2_slots bytes on the current device,
+ * create: allocates 48 * 2^log2_slots bytes (32-byte keys, 8-byte tags,
+ * 8-byte recency words) plus a small metadata block on the current device,
  * cleared.  log2_slots in [4, 31].  Errors: KVGOV_E_INVAL, KVGOV_E_NOMEM,
  * KVGOV_E_HIP.  The cache must be used with that device current
  * (KVGOV_E_DEVICE otherwise).
@@ -322,7 +323,7 @@ int kvgov_cache_erase(kvgov_cache *c, const uint8_t *keys, int64_t n_keys, int64
  * below its parent: match = 16 * (block depth) + (tokens matched in the next
  * block).
  *
- * create: block table of 2^log2_block_slots slots (~40 B each) and edge
+ * create: block table of 2^log2_block_slots slots (48 B each) and edge
  * table of 2^log2_edge_slots slots (8 B each; up to 15 edges per distinct
  * block, fewer where sequences share token prefixes), both in [4, 30], on the
  * current device (which must be current for every later call:
