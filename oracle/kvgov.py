@@ -14,9 +14,10 @@ Readings of the paper taken here (each also listed in the design notes):
 * Boundary salting (Sec. 4.2 display): blocks j < k unsalted,
   h_k = SHA256(sigma_p || h_{k-1} || T_k), blocks after k chained.  k is
   given per request as a token offset, k = boundary_tok // B (Sec. 5.6: a
-  divergence at token i invalidates every block from floor(i/B)); k = 0 has
+  prompt that first differs at token i keeps no block from floor(i/B) on); k = 0 has
   no parent and is SHA256(sigma_p || T_0), the root-salted case; k at or
-  beyond the last full block salts nothing (Sec. 4.2, "all-or-nothing").
+  beyond the last full block salts nothing (Sec. 4.2 places root salting
+  at one end of the range of boundaries).
 * Only full blocks are hashed, inserted and probed; a trailing partial block
   is ignored (Sec. 2.1: matches are truncated to a block boundary).
 * Lookup returns the index of the first block whose hash is not in the table
