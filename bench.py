@@ -26,7 +26,11 @@ value = block tokens hashed per second over the whole step (16 tokens per
 full block, both batches, both modes); lookups/s and block hashes/s are
 reported beside it.  The roofline entry is for the chain-hashing kernel,
 the dominant kernel of the step, timed with HIP events on its own stream;
-the lookup kernel's HBM roofline is reported beside it.
+the lookup kernel's HBM roofline is reported beside it.  The timed steps
+carry HIP events around the chain launches only (a timing event costs its
+stream a few microseconds: events around every call made the paper-shaped
+step 0.78 instead of 0.74 ms); the per-phase launch times come from as many
+steps again, run after the timed ones with events around every call.
 
 Beside the bench line's own fields: per-phase rates for every mode (median,
 mean and min launch times of salts, chains, clear, insert, lookup, with
@@ -818,7 +822,11 @@ def main():
         ev.record(sst)
         salted_evs[k % 2] = ev
 
-    def step(record: bool, i: int):
+    def step(i: int, chains_ev: bool, phase_ev: bool):
+        """Step i.  chains_ev: timing events around the dominant launches
+        (the chains; the probe workload's lookups); phase_ev: timing events
+        around every other call.  Each timing event costs the stream a few
+        microseconds, so the timed steps carry only the first kind."""
         nonlocal salts
         st = use_set(i % depth)
         sst = st["sstream"]
@@ -833,7 +841,7 @@ def main():
             for ev in st["chains_done"] + (st["step_done"] if depth == 1 else []):
                 sst.wait_event(ev)
             if not probe_only:
-                end = timed(ev_salts, None, sst) if record else None
+                end = timed(ev_salts, None, sst) if phase_ev else None
                 K.salts(wl.K, ids, out=salts, stream=sst)
                 if end:
                     end()
@@ -846,13 +854,13 @@ def main():
             hA, hB = bview(m)
             if not probe_only:
                 # the table clear needs no salts: it overlaps the salts kernel
-                end = timed(ev_clear, m, s) if record else None
+                end = timed(ev_clear, m, s) if phase_ev else None
                 (radixes if radix_cfg else caches)[m].clear(stream=s)
                 if end:
                     end()
             s.wait_event(salted)
             if not probe_only:
-                if record:
+                if chains_ev:
                     e0 = torch.cuda.Event(enable_timing=True)
                     e1 = torch.cuda.Event(enable_timing=True)
                     e0.record(s)
@@ -860,7 +868,7 @@ def main():
                 cd = torch.cuda.Event()
                 cd.record(s)
                 st["chains_done"].append(cd)
-                if record:
+                if chains_ev:
                     e1.record(s)
                     ev_chain.append((m, e0, e1))
                 if radix_cfg:
@@ -868,50 +876,51 @@ def main():
                     # the concatenated arrays: A's requests come first)
                     pr = x["principal"] if m != W.NONE else None
                     sd = salts if m != W.NONE else None
-                    end = timed(ev_rins, m, s) if record else None
+                    end = timed(ev_rins, m, s) if phase_ev else None
                     radixes[m].insert(x["tokens"], x["tok_offsets"][:A.n + 1],
                                       None if pr is None else pr[:A.n], sd, m, out[m],
                                       x["blk_offsets"][:A.n + 1], stream=s)
                     if end:
                         end()
-                    end = timed(ev_rmatch, m, s) if record else None
+                    end = timed(ev_rmatch, m, s) if phase_ev else None
                     radixes[m].match(x["tokens"], x["tok_offsets"][A.n:],
                                      None if pr is None else pr[A.n:], sd, m, out[m],
                                      x["blk_offsets"][A.n:], out=matched[m], stream=s)
                     if end:
                         end()
                 elif admission:
-                    end = timed(ev_adm, m, s) if record else None
+                    end = timed(ev_adm, m, s) if phase_ev else None
                     caches[m].admit(out[m], x["blk_offsets"], sync=False, hits=adm_hits[m],
                                     new=adm_new[m], stream=s)
                     if end:
                         end()
                 else:
-                    end = timed(ev_ins, m, s) if record else None
+                    end = timed(ev_ins, m, s) if phase_ev else None
                     caches[m].insert(hA, boA, sync=False, stream=s)
                     if end:
                         end()
                 if maint_cfg:
                     # the second insert call, then the maintenance calls
-                    end = timed(ev_ins_b, m, s) if record else None
+                    end = timed(ev_ins_b, m, s) if phase_ev else None
                     caches[m].insert(hB, boB, sync=False, stream=s)
                     if end:
                         end()
-                    end = timed(ev_evict, m, s) if record else None
+                    end = timed(ev_evict, m, s) if phase_ev else None
                     caches[m].evict(max_keys[m], sync=False, stream=s)
                     if end:
                         end()
-                    end = timed(ev_erase, m, s) if record else None
+                    end = timed(ev_erase, m, s) if phase_ev else None
                     caches[m].erase(hA[:n_erase], sync=False, stream=s)
                     if end:
                         end()
             if not admission and not radix_cfg:
-                if record:
+                rec_look = chains_ev if probe_only else phase_ev
+                if rec_look:
                     l0 = torch.cuda.Event(enable_timing=True)
                     l1 = torch.cuda.Event(enable_timing=True)
                     l0.record(s)
                 caches[m].lookup(hB, boB, out=hits[m], stream=s)
-                if record:
+                if rec_look:
                     l1.record(s)
                     ev_look.append((m, l0, l1))
             ev = torch.cuda.Event()
@@ -921,21 +930,30 @@ def main():
         if early:
             readers[i % 2] = list(st["chains_done"])
             salted_evs[i % 2] = None
-            enqueue_salts(i + 1, record)
+            enqueue_salts(i + 1, phase_ev)
 
     log(f"warmup {args.warmup} steps ({depth} batch(es) in flight)")
     for i in range(args.warmup):
-        step(False, i)
+        step(i, False, False)
     torch.cuda.synchronize()
     log(f"timing {args.steps} steps")
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(True, args.warmup + i)
+        step(args.warmup + i, True, False)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     t_step = elapsed / args.steps
+    last = args.warmup + args.steps - 1
+    if not probe_only:
+        # the per-phase launch times: as many steps again, after the timed
+        # ones, with events around every call
+        log(f"{args.steps} more steps with per-phase events")
+        for i in range(args.steps):
+            step(args.warmup + args.steps + i, False, True)
+        torch.cuda.synchronize()
+        last += args.steps
     # the results below are those of the last step's buffer set
-    use_set((args.warmup + args.steps - 1) % depth)
+    use_set(last % depth)
 
     # ---- gates: latched errors, bit-exactness on a sample, by-construction hits
     K.check_status(status, "bench step")
