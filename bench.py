@@ -865,12 +865,16 @@ def main():
                     e1 = torch.cuda.Event(enable_timing=True)
                     e0.record(s)
                 hash_call(m, s)
-                cd = torch.cuda.Event()
-                cd.record(s)
-                st["chains_done"].append(cd)
+                # the chains' end (the salts buffer they read may be
+                # rewritten after it); the timing event serves when there is one
                 if chains_ev:
                     e1.record(s)
                     ev_chain.append((m, e0, e1))
+                    cd = e1
+                else:
+                    cd = torch.cuda.Event()
+                    cd.record(s)
+                st["chains_done"].append(cd)
                 if radix_cfg:
                     # insert batch A's sequences, match batch B's (views of
                     # the concatenated arrays: A's requests come first)
@@ -923,9 +927,11 @@ def main():
                 if rec_look:
                     l1.record(s)
                     ev_look.append((m, l0, l1))
-            ev = torch.cuda.Event()
-            ev.record(s)
-            done.append(ev)
+            if not early or depth > 1:
+                # waited on by the next step's salts (derived in the step)
+                ev = torch.cuda.Event()
+                ev.record(s)
+                done.append(ev)
         st["step_done"] = done
         if early:
             readers[i % 2] = list(st["chains_done"])
