@@ -149,6 +149,29 @@ def test_chains_many_waves_and_ordering(mode):
     assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("mode", [W.ROOT, W.BOUNDARY])
+def test_chains_long_with_scattered_boundaries(mode):
+    """Long chains (94..200 blocks) whose boundaries fall on different blocks
+    across each 64-request workgroup, some on the first or last block or
+    past it: the lane-pair kernel switches between the first compression's
+    precomputed schedule terms and the plain schedule at every iteration
+    where some request of the workgroup has its boundary block."""
+    g = np.random.default_rng(41)
+    lens = g.integers(1500, 3200, 256)
+    b = ragged(43 + mode, lens, P=9)
+    bt = b.boundary_tok
+    L = b.lengths
+    for i in range(0, 256, 16):
+        bt[i] = 0
+        bt[i + 1] = (L[i + 1] // 16) * 16 - 16  # the last full block
+        bt[i + 2] = L[i + 2]
+    Kb, ids = secret(8, 9)
+    got = gpu_chains(b, K.salts(Kb, dev(ids)), mode).cpu().numpy()
+    want = O.hash_chains_parallel(b.tokens, b.tok_offsets, b.principal, O.salts(Kb, ids), mode,
+                                  bt)
+    assert np.array_equal(got, want)
+
+
 def test_chains_unaligned_token_offsets():
     """Requests starting at any token offset (tokens not 16-byte aligned)."""
     b = ragged(41, [1, 35, 2, 70, 3, 17, 5, 64])
