@@ -751,15 +751,85 @@ __device__ __forceinline__ void lp_step2(uint32_t s[4], uint32_t &z, uint32_t kw
   z = zb;
 }
 
+// Runs of 6, 14 or 16 steps as one asm statement: the compiler puts a wait
+// state between consecutive asm statements (it cannot see that their DPP
+// sources are old), which cost about a cycle per step with two-step
+// statements.  The four words x0..x3 live in a ring of four registers q0..q3
+// (step k reads x0 from q[-k mod 4] and writes x0' over the dead x3), Z
+// alternates between y0 and y1, and six temporaries are reused by every
+// step.  After a multiple of four steps the ring is back in place; after
+// 4k + 2 steps x0..x3 sit in q2, q3, q0, q1.
+#define KVGOV_LP_RING_T "%[t1]", "%[t2]", "%[t3]", "%[x]", "%[f]", "%[sg]"
+#define KVGOV_LP_STEP_(...) KVGOV_LP_STEP(__VA_ARGS__)
+#define KVGOV_LP_R0(K) KVGOV_LP_STEP_("%[q0]", "%[q1]", "%[q2]", "%[y0]", "%[q3]", "%[y1]", K, KVGOV_LP_RING_T)
+#define KVGOV_LP_R1(K) KVGOV_LP_STEP_("%[q3]", "%[q0]", "%[q1]", "%[y1]", "%[q2]", "%[y0]", K, KVGOV_LP_RING_T)
+#define KVGOV_LP_R2(K) KVGOV_LP_STEP_("%[q2]", "%[q3]", "%[q0]", "%[y0]", "%[q1]", "%[y1]", K, KVGOV_LP_RING_T)
+#define KVGOV_LP_R3(K) KVGOV_LP_STEP_("%[q1]", "%[q2]", "%[q3]", "%[y1]", "%[q0]", "%[y0]", K, KVGOV_LP_RING_T)
+#define KVGOV_LP_RING4(A, B, C, D) KVGOV_LP_R0(A) KVGOV_LP_R1(B) KVGOV_LP_R2(C) KVGOV_LP_R3(D)
+#define KVGOV_LP_RING_OUT                                                                    \
+  [q0] "+v"(s[0]), [q1] "+v"(s[1]), [q2] "+v"(s[2]), [q3] "+v"(s[3]), [y0] "+v"(z),         \
+      [y1] "=&v"(y1), [t1] "=&v"(t1), [t2] "=&v"(t2), [t3] "=&v"(t3), [x] "=&v"(x),          \
+      [f] "=&v"(f), [sg] "=&v"(sg)
+#define KVGOV_LP_RING_IN [m] "v"(c.m), [r1] "v"(c.r1), [r2] "v"(c.r2), [r3] "v"(c.r3)
+#define KVGOV_LP_K(i) [k##i] "v"(k[i - 1])
+
+// k[i] is the kw taken by step i (the next step's)
+template <int N>
+__device__ __forceinline__ void lp_ring(uint32_t s[4], uint32_t &z, const uint32_t k[N],
+                                        const LpLane &c) {
+  static_assert(N == 6 || N == 14 || N == 16, "ring runs of 6, 14 or 16 steps");
+  uint32_t y1, t1, t2, t3, x, f, sg;
+  if constexpr (N == 16) {
+    asm(KVGOV_LP_RING4("%[k1]", "%[k2]", "%[k3]", "%[k4]")
+        KVGOV_LP_RING4("%[k5]", "%[k6]", "%[k7]", "%[k8]")
+        KVGOV_LP_RING4("%[k9]", "%[k10]", "%[k11]", "%[k12]")
+        KVGOV_LP_RING4("%[k13]", "%[k14]", "%[k15]", "%[k16]")
+        : KVGOV_LP_RING_OUT
+        : KVGOV_LP_RING_IN, KVGOV_LP_K(1), KVGOV_LP_K(2), KVGOV_LP_K(3), KVGOV_LP_K(4),
+          KVGOV_LP_K(5), KVGOV_LP_K(6), KVGOV_LP_K(7), KVGOV_LP_K(8), KVGOV_LP_K(9),
+          KVGOV_LP_K(10), KVGOV_LP_K(11), KVGOV_LP_K(12), KVGOV_LP_K(13), KVGOV_LP_K(14),
+          KVGOV_LP_K(15), KVGOV_LP_K(16));
+  } else if constexpr (N == 14) {
+    asm(KVGOV_LP_RING4("%[k1]", "%[k2]", "%[k3]", "%[k4]")
+        KVGOV_LP_RING4("%[k5]", "%[k6]", "%[k7]", "%[k8]")
+        KVGOV_LP_RING4("%[k9]", "%[k10]", "%[k11]", "%[k12]")
+        KVGOV_LP_R0("%[k13]") KVGOV_LP_R1("%[k14]")
+        : KVGOV_LP_RING_OUT
+        : KVGOV_LP_RING_IN, KVGOV_LP_K(1), KVGOV_LP_K(2), KVGOV_LP_K(3), KVGOV_LP_K(4),
+          KVGOV_LP_K(5), KVGOV_LP_K(6), KVGOV_LP_K(7), KVGOV_LP_K(8), KVGOV_LP_K(9),
+          KVGOV_LP_K(10), KVGOV_LP_K(11), KVGOV_LP_K(12), KVGOV_LP_K(13), KVGOV_LP_K(14));
+  } else {
+    asm(KVGOV_LP_RING4("%[k1]", "%[k2]", "%[k3]", "%[k4]")
+        KVGOV_LP_R0("%[k5]") KVGOV_LP_R1("%[k6]")
+        : KVGOV_LP_RING_OUT
+        : KVGOV_LP_RING_IN, KVGOV_LP_K(1), KVGOV_LP_K(2), KVGOV_LP_K(3), KVGOV_LP_K(4),
+          KVGOV_LP_K(5), KVGOV_LP_K(6));
+  }
+  if constexpr (N % 4 == 2) {
+    const uint32_t w0 = s[2], w1 = s[3], w2 = s[0], w3 = s[1];
+    s[0] = w0;
+    s[1] = w1;
+    s[2] = w2;
+    s[3] = w3;
+  }
+}
+
 // N steps; kw holds the group's own kw (kw[0] is already in z), kw_after
 // the kw of the step after the group
 template <int N>
 __device__ __forceinline__ void lp_steps(uint32_t s[4], uint32_t &z, const uint32_t *kw,
                                          uint32_t kw_after, const LpLane &c) {
+  if constexpr (N == 6 || N == 14 || N == 16) {
+    uint32_t k[N];
 #pragma unroll
-  for (int i = 0; i + 1 < N; i += 2)
-    lp_step2(s, z, kw[i + 1], i + 2 < N ? kw[i + 2] : kw_after, c);
-  if (N & 1) lp_step(s, z, kw_after, c);
+    for (int i = 0; i < N; ++i) k[i] = i + 1 < N ? kw[i + 1] : kw_after;
+    lp_ring<N>(s, z, k, c);
+  } else {
+#pragma unroll
+    for (int i = 0; i + 1 < N; i += 2)
+      lp_step2(s, z, kw[i + 1], i + 2 < N ? kw[i + 2] : kw_after, c);
+    if (N & 1) lp_step(s, z, kw_after, c);
+  }
 }
 
 // steps 0 and 1 of a compression: the A lane's results are replaced by the
