@@ -390,16 +390,24 @@ def test_cache_insert_ignores_interior_offsets():
         assert key_set(c.export().cpu().numpy()) == key_set(keys)
 
 
-@pytest.mark.parametrize("n_req", [1, 7, 64, 5000, 20000, 300000])
+@pytest.mark.parametrize("n_req", [1, 7, 64, 3000, 5000, 20000, 300000])
 def test_cache_lookup_group_sizes(n_req):
-    """Lookups at batch sizes that select every lanes-per-request width."""
+    """Lookups at batch sizes that select every lanes-per-request width
+    (3000 long requests: many rounds per request, first misses at chosen
+    positions)."""
     g = np.random.default_rng(n_req)
-    # long requests at 20000 (lanes per request from the average length)
-    nb = g.integers(0, 400 if n_req == 20000 else 70, n_req).astype(np.int64)
+    # long requests at 20000 and 3000 (lanes per request from the average length)
+    hi = {20000: 400, 3000: 900}.get(n_req, 70)
+    nb = g.integers(0, hi, n_req).astype(np.int64)
+    edge = [0, 1, 255, 256, 257, 511, 512, 513, 767, 768, 799, 800, 800, 100]
+    if n_req == 3000:
+        nb[:len(edge)] = 800  # first misses at the rounds' edges, and none
     bo = np.concatenate([[0], np.cumsum(nb)])
     keys = g.integers(0, 256, (int(bo[-1]), 32), dtype=np.uint8)
     # insert a random prefix of each request's keys
     pre = np.floor(g.random(n_req) * (nb + 1)).astype(np.int64)
+    if n_req == 3000:
+        pre[:len(edge)] = edge
     ins = np.concatenate([keys[bo[r]:bo[r] + pre[r]] for r in range(n_req)] +
                          [np.zeros((0, 32), np.uint8)])
     with K.Cache(max(6, int(np.ceil(np.log2(max(ins.shape[0], 1) * 2 + 1))))) as c:
