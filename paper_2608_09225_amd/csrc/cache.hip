@@ -110,7 +110,9 @@ __device__ __forceinline__ int32_t find_request(const int64_t *bo, int32_t n, in
 // (the earlier one is inserted, or is itself a duplicate of an earlier
 // one), and the compared position is checked to lie in the batch, so
 // malformed interior offsets cannot cause a wrong result or an
-// out-of-range read.
+// out-of-range read.  A row's request, and so its depth (its position in
+// the request, which the recency rank holds), is exact: rows whose request
+// lies past the window search for it.
 //
 // ADMIT: also the admission's first half: claims are lowered to the
 // earliest row, and codes[f] records where row f's key went (kCodeDup for a
@@ -151,9 +153,20 @@ __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hash
         const int64_t v = __shfl(win, cand < 63 ? cand : 63, 64);
         if (cand <= 63 && v <= f) pos = cand;
       }
-      const int64_t b_r = __shfl(win, pos, 64);
-      const int64_t b_p = __shfl(win, pos - 1, 64);
-      const int32_t r = rc - 1 + pos;
+      int64_t b_r = __shfl(win, pos, 64);
+      int64_t b_p = __shfl(win, pos - 1, 64);
+      int32_t r = rc - 1 + pos;
+      if (pos == 63) {
+        // 64 rows can span more requests than the window reaches (requests
+        // of one block or none): a row whose request starts past the window
+        // finds it by binary search (its depth depends on it)
+        const int32_t ne = rc + 63;
+        if (ne < n && blk_offsets[ne] <= f) {
+          r = find_request(blk_offsets, n, f);
+          b_r = blk_offsets[r];
+          b_p = blk_offsets[r - 1];
+        }
+      }
       if (f < f1) {
         const Key key = load_key(hashes + f * 32);
         bool dup = false;

@@ -163,3 +163,18 @@ def test_untracked_table_erases_but_does_not_evict():
         c.insert(dev(h[100:150]), dev(np.array([0, 50], np.int64)))
         assert c.evict(50) == 50
         assert key_set(c.export()) == {h[i].tobytes() for i in range(100, 150)}
+
+
+@pytest.mark.parametrize("empties", [False, True])
+def test_depth_when_a_stretch_spans_many_requests(empties):
+    """Every key of a batch of one-block requests (with an empty request
+    before each, or not) sits at depth 0, so the batch is one rank class:
+    64 consecutive rows then span more requests than a window of 64 request
+    starts reaches, and a wrong depth would split the class and change what
+    an eviction keeps."""
+    n = 1000
+    keys = arr([key_of(i) for i in range(n)])
+    bo = np.repeat(np.arange(n + 1), 2)[:2 * n + 1] if empties else np.arange(n + 1)
+    bo = bo.astype(np.int64)
+    replay([("insert", (keys, bo)), ("evict", n - 1), ("insert", (keys, bo)),
+            ("evict", n)], log2_slots=12)
