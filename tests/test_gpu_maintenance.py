@@ -165,8 +165,9 @@ def test_untracked_table_erases_but_does_not_evict():
         assert key_set(c.export()) == {h[i].tobytes() for i in range(100, 150)}
 
 
+@pytest.mark.parametrize("op", ["insert", "admit"])
 @pytest.mark.parametrize("empties", [False, True])
-def test_depth_when_a_stretch_spans_many_requests(empties):
+def test_depth_when_a_stretch_spans_many_requests(empties, op):
     """Every key of a batch of one-block requests (with an empty request
     before each, or not) sits at depth 0, so the batch is one rank class:
     64 consecutive rows then span more requests than a window of 64 request
@@ -176,5 +177,5 @@ def test_depth_when_a_stretch_spans_many_requests(empties):
     keys = arr([key_of(i) for i in range(n)])
     bo = np.repeat(np.arange(n + 1), 2)[:2 * n + 1] if empties else np.arange(n + 1)
     bo = bo.astype(np.int64)
-    replay([("insert", (keys, bo)), ("evict", n - 1), ("insert", (keys, bo)),
-            ("evict", n)], log2_slots=12)
+    replay([(op, (keys, bo)), ("evict", n - 1), (op, (keys, bo)), ("evict", n)],
+           log2_slots=12)
