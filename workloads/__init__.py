@@ -18,13 +18,19 @@ Workload shapes follow the paper's setting:
 
 The paper's prompts and templates are not published; every array here is a
 seeded stand-in with the stated shape.  Streams are independent: each named
-stream gets ``np.random.SeedSequence([seed, *name.encode()])`` with the master
-seed 2026 (the paper's seed, Sec. 5.1).
+stream ``<config>/<name>`` gets ``np.random.default_rng([seed, s])`` with the
+master seed 2026 (the paper's seed, Sec. 5.1) and s the first 8 bytes,
+little-endian, of the SHA-256 digest of the stream's name (the paper derives
+each condition's stream from a SHA-256 digest of the condition's name, Sec. 7,
+reproducibility paragraph).  That digest of a name is the only hashing here:
+no token, block, salt or chain is hashed.
 """
 from __future__ import annotations
 
 from dataclasses import dataclass, field
 from typing import Dict, List, Optional
+
+import hashlib
 
 import numpy as np
 
@@ -37,9 +43,15 @@ NONE, ROOT, BOUNDARY = 0, 1, 2
 MODE_NAMES = {NONE: "none", ROOT: "root", BOUNDARY: "boundary"}
 
 
+def stream_seed(name: str) -> int:
+    """The per-stream half of a generator's seed: the first 8 bytes of
+    SHA-256(name), read little-endian."""
+    return int.from_bytes(hashlib.sha256(name.encode()).digest()[:8], "little")
+
+
 def rng(name: str, seed: int = SEED) -> np.random.Generator:
     """Independent generator for the stream ``name``."""
-    return np.random.default_rng(np.random.SeedSequence([seed, *name.encode()]))
+    return np.random.default_rng([seed, stream_seed(name)])
 
 
 @dataclass
@@ -272,13 +284,14 @@ def probe(seed: int = SEED, n_res: int = 250_000, n_probe: int = 1_000_000,
     lens = nblk * BLOCK
     offs = _flat(lens)
     toks = _uniform_tokens(g, int(offs[-1]))
-    # copy the shared prefix: probe tokens [0, 16 d) <- resident tokens [0, 16 d)
-    ncopy = d * BLOCK
-    dst_start = np.repeat(offs[:-1], ncopy)
-    src_start = np.repeat(src * L_res, ncopy)
-    within = np.arange(int(ncopy.sum()), dtype=np.int64) - np.repeat(
-        np.cumsum(ncopy) - ncopy, ncopy)
-    toks[dst_start + within] = res_toks[src_start + within]
+    # copy the shared prefix: probe blocks [0, d) <- resident blocks [0, d)
+    # (every probe starts on a block edge, so whole 16-token rows are copied)
+    blk = toks.reshape(-1, BLOCK)
+    res_blk = res_toks.reshape(-1, BLOCK)
+    first = np.repeat(offs[:-1] // BLOCK - (np.cumsum(d) - d), d)
+    within = np.arange(int(d.sum()), dtype=np.int64)
+    src_first = np.repeat(src * (L_res // BLOCK) - (np.cumsum(d) - d), d)
+    blk[first + within] = res_blk[src_first + within]
     # force divergence at token 16 d when the probe and the resident request
     # both have a block d
     div = (d < nblk) & (d < 32)
