@@ -3,23 +3,31 @@ uses (one hashing call per batch and mode, the table sizes of the configs).
 
 * tiny, paper, template: every digest, every hit count and n_new against the
   oracle.
-* probe (8M resident keys, 1M probes): sampled requests' digests against the
-  oracle; every hit count against the value fixed by construction (d for a
-  probe copying d blocks under its own principal, 0 under another principal),
-  and for sampled probes against the oracle's own lookup in its source chain.
-* large (65,536 requests, 13.7M blocks per mode): sampled requests (including
-  the longest) against the oracle; at full size, properties that hold at any
-  size: all keys distinct so n_new equals the block count, and a lookup of the
-  inserted batch hits every block.
+* probe (8M resident keys, 1M probes): every digest of both batches against
+  the oracle, every hit count against the oracle's lookup of its own probe
+  digests in its own resident set, and against the value fixed by
+  construction (d for a probe copying d blocks under its own principal, 0
+  under another principal).
+* large (65,536 requests, 13.7M blocks per mode): every digest of both modes
+  against the oracle; n_new and every hit count of the re-lookup against the
+  oracle's (all keys distinct, so a lookup of the inserted batch hits every
+  block).
 * session (4096 two-turn sessions): turn 2's chains resumed from turn 1's
   last digests, every digest, n_new and hit count against the oracle's own
   resumed chains.
 * admission, radix, maintenance (the paper-shaped batches on the three
   later stages, one call shape each as bench.py times them): every admitted
   request's hits and new blocks against the oracle's sequential admission;
-  sampled token-granular matches against the oracle's index and every match
-  against the shared prefix; the maintained table (two tracked inserts, an
-  eviction to half, an erase, a re-lookup) replayed by the oracle.
+  every token-granular match against the oracle's index (root: per-principal
+  trees; unsalted: 256 sampled requests, since each is compared with all 4096
+  sequences) and every match against the shared prefix; the maintained table
+  (two tracked inserts, an eviction to half, an erase, a re-lookup) replayed
+  by the oracle.
+
+The probe and large workloads are compared in request ranges on forked worker
+processes: each worker hashes its range with the oracle and compares it with
+the same rows of the GPU output (copied to host memory before the fork), so
+no process holds a whole batch's oracle digests at once.
 """
 import hashlib
 import os
@@ -72,6 +80,71 @@ def rows_of(b, hashes_np, r):
         _BO[id(b)] = (b, b.blk_offsets())
     bo = _BO[id(b)][1]
     return hashes_np[bo[r]:bo[r + 1]]
+
+
+# ---------------------------------------------------------------------------
+# whole-batch comparisons on worker processes
+# ---------------------------------------------------------------------------
+
+_SHARED = {}
+
+
+def _ranges(n, procs, per_proc=8):
+    step = max(1, -(-n // (procs * per_proc)))
+    return [(a, min(a + step, n)) for a in range(0, n, step)]
+
+
+def _cmp_range(rng_):
+    """Oracle digests of requests [a, b) against the GPU rows of the same
+    requests; with a resident key set, also the oracle's lookup of those
+    digests against the GPU hit counts.  Returns (a, b, bad request or -1,
+    bad hit request or -1)."""
+    a, b = rng_
+    sh = _SHARED
+    bt, bo = sh["batch"], sh["bo"]
+    want = O.hash_chains(bt.tokens, bt.tok_offsets, bt.principal, sh["salts"], sh["mode"],
+                         bt.boundary_tok, requests=range(a, b))
+    got = sh["gpu"][bo[a]:bo[b]]
+    bad = -1
+    if not np.array_equal(got, want):
+        for r in range(a, b):
+            if not np.array_equal(got[bo[r]:bo[r + 1]], want[bo[r] - bo[a]:bo[r + 1] - bo[a]]):
+                bad = r
+                break
+    bad_hit = -1
+    if sh.get("keys") is not None:
+        local = bo[a:b + 1] - bo[a]
+        hits = O.lookup_hits(sh["keys"], want, local)
+        diff = np.nonzero(hits != sh["hits"][a:b])[0]
+        bad_hit = int(a + diff[0]) if diff.size else -1
+    return a, b, bad, bad_hit
+
+
+def key_set(rows):
+    """The rows of a uint8 [n, 32] array as a set of 32-byte keys."""
+    raw = np.ascontiguousarray(rows).tobytes()
+    return {raw[i:i + 32] for i in range(0, len(raw), 32)}
+
+
+def compare_all(b, osalts, mode, gpu_rows, keys=None, gpu_hits=None):
+    """Every request of ``b``: the oracle's chains against ``gpu_rows`` (host
+    uint8 [rows, 32]) and, given a key set, the oracle's lookup hits against
+    ``gpu_hits``."""
+    import multiprocessing as mp
+    bo = b.blk_offsets()
+    assert gpu_rows.shape == (int(bo[-1]), 32)
+    _SHARED.update(batch=b, bo=bo, salts=osalts, mode=mode, gpu=gpu_rows, keys=keys,
+                   hits=gpu_hits)
+    try:
+        with mp.get_context("fork").Pool(PROCS) as pool:
+            res = pool.map(_cmp_range, _ranges(b.n, PROCS))
+    finally:
+        _SHARED.clear()
+    bad = [r for _, _, r, _ in res if r >= 0]
+    assert not bad, f"digests of request {bad[0]} differ from the oracle"
+    bad_hit = [r for _, _, _, r in res if r >= 0]
+    assert not bad_hit, f"hit count of request {bad_hit[0]} differs from the oracle"
+    assert sum(y - x for x, y, _, _ in res) == b.n
 
 
 def full_pipeline(wl, mode):
@@ -134,6 +207,9 @@ def probe_wl():
 
 
 def test_probe_config(probe_wl):
+    """Every resident and probe digest against the oracle, n_new, and every
+    probe's hit count against the oracle's first-miss lookup in the oracle's
+    resident key set (and the value fixed by construction)."""
     wl = probe_wl
     res, pr = wl.insert, wl.lookup
     sd = K.salts(wl.K, dev(wl.principal_ids))
@@ -144,15 +220,18 @@ def test_probe_config(probe_wl):
         assert c.slots() == 1 << 24
         n_new = c.insert(h_res, dev(res.blk_offsets()))
         hits = c.lookup(h_pr, dev(pr.blk_offsets())).cpu().numpy()
-    assert n_new == res.n * 32  # random 512-token prompts: every key distinct
     assert np.array_equal(hits, pr.expect_hits[W.ROOT])
-    # sampled digests against the oracle
-    g = np.random.default_rng(5)
-    hr, hp = h_res.cpu().numpy(), h_pr.cpu().numpy()
-    for r in g.choice(res.n, 300, replace=False):
-        assert np.array_equal(rows_of(res, hr, r), oracle_chains(res, osalts, W.ROOT, [int(r)]))
-    for p in g.choice(pr.n, 300, replace=False):
-        assert np.array_equal(rows_of(pr, hp, p), oracle_chains(pr, osalts, W.ROOT, [int(p)]))
+    hr = h_res.cpu().numpy()
+    del h_res
+    # resident chains: every digest; the oracle's key set is built from its
+    # own digests, which equal the GPU's once the comparison has passed
+    compare_all(res, osalts, W.ROOT, hr)
+    keys = key_set(hr)
+    assert n_new == len(keys) == res.n * 32  # random 512-token prompts: all distinct
+    del hr
+    hp = h_pr.cpu().numpy()
+    del h_pr
+    compare_all(pr, osalts, W.ROOT, hp, keys=keys, gpu_hits=hits)
 
 
 def test_probe_sources_checked_by_oracle(probe_wl):
@@ -188,6 +267,8 @@ def large_wl():
 
 @pytest.mark.parametrize("mode", [W.ROOT, W.BOUNDARY])
 def test_large_config(large_wl, mode):
+    """Every digest of the 65,536-request batch against the oracle; the
+    insert's n_new and every hit of the re-lookup against the oracle's."""
     wl = large_wl
     b = wl.insert
     sd = K.salts(wl.K, dev(wl.principal_ids))
@@ -195,15 +276,17 @@ def test_large_config(large_wl, mode):
     h = gpu_chains(b, sd, mode)
     nb = int(b.block_counts().sum())
     with K.Cache(wl.log2_slots) as c:
-        assert c.insert(h, dev(b.blk_offsets())) == nb  # all keys distinct
+        n_new = c.insert(h, dev(b.blk_offsets()))
         hits = c.lookup(h, dev(b.blk_offsets())).cpu().numpy()
-    assert np.array_equal(hits, b.block_counts())
     hn = h.cpu().numpy()
-    g = np.random.default_rng(7)
-    longest = np.argsort(-b.lengths)[:16]
-    sample = np.concatenate([longest, g.choice(b.n, 400, replace=False)])
-    for r in sample:
-        assert np.array_equal(rows_of(b, hn, r), oracle_chains(b, osalts, mode, [int(r)])), r
+    del h
+    # the key set is built from the GPU rows before the workers fork; the
+    # workers first compare those rows with the oracle's, so once the call
+    # returns it is the oracle's set
+    keys = key_set(hn)
+    compare_all(b, osalts, mode, hn, keys=keys, gpu_hits=hits)
+    assert n_new == len(keys) == nb  # all keys distinct
+    assert np.array_equal(hits, b.block_counts())
 
 
 def test_many_requests_longest_first_ordering():
@@ -324,8 +407,9 @@ def radix_wl():
 def test_radix_config(radix_wl, mode):
     """The insert batch's sequences into the radix index (2^23 edge slots, as
     bench.py), the re-lookup batch matched: every match covers the shared
-    2119-token prefix, 96 sampled matches equal the oracle's, and the index
-    holds one block node per distinct digest plus its roots."""
+    2119-token prefix and equals the oracle's (root salting; 256 sampled
+    requests unsalted), and the index holds one block node per distinct
+    digest plus its roots."""
     wl = radix_wl
     A, B = wl.insert, wl.lookup
     sd = K.salts(wl.K, dev(wl.principal_ids))
@@ -346,11 +430,34 @@ def test_radix_config(radix_wl, mode):
     ha = oracle_chains_cached(A, osalts, mode)
     roots = wl.P if salted else 1  # a root per salt of the table, or the zero root
     assert blocks == roots + len({ha[i].tobytes() for i in range(ha.shape[0])})
-    qs = np.sort(np.random.default_rng(17).choice(B.n, 96, replace=False))
     R = O.Radix()
     R.insert(A.tokens, A.tok_offsets, A.principal, osalts, mode)
-    want = R.match(B.tokens, B.tok_offsets, B.principal, osalts, mode, requests=qs)
+    # root: every request (a request is compared with its principal's
+    # sequences only); unsalted: 256 sampled requests, each compared with all
+    # 4096 inserted sequences
+    qs = np.arange(B.n) if salted else \
+        np.sort(np.random.default_rng(17).choice(B.n, 256, replace=False))
+    want = radix_match_parallel(R, B, osalts, mode, qs)
     assert np.array_equal(got[qs], want)
+
+
+def _radix_range(rng_):
+    a, b = rng_
+    sh = _SHARED
+    return sh["R"].match(sh["B"].tokens, sh["B"].tok_offsets, sh["B"].principal, sh["salts"],
+                         sh["mode"], requests=sh["qs"][a:b])
+
+
+def radix_match_parallel(R, B, osalts, mode, qs):
+    """The oracle index's matches of requests ``qs``, split over workers."""
+    import multiprocessing as mp
+    _SHARED.update(R=R, B=B, salts=osalts, mode=mode, qs=qs)
+    try:
+        with mp.get_context("fork").Pool(PROCS) as pool:
+            parts = pool.map(_radix_range, _ranges(len(qs), PROCS))
+    finally:
+        _SHARED.clear()
+    return np.concatenate(parts)
 
 
 @pytest.fixture(scope="module")
