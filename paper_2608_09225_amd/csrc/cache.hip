@@ -470,7 +470,10 @@ __global__ __launch_bounds__(256) void k_gather_ranks(TableView t, SelectState *
       mn = a < mn ? a : mn;
       mx = b > mx ? b : mx;
     }
-    if ((threadIdx.x & 63) == 0 && mx) {
+    // a wave holding keys reports its range even when every word is 0 (keys
+    // inserted while tracking was off): the select must see that class too
+    const bool any = __ballot(have != 0) != 0;
+    if ((threadIdx.x & 63) == 0 && any) {
       atomicMin(&st->lo, mn);
       atomicMax(&st->hi, mx);
     }

@@ -179,3 +179,27 @@ def test_depth_when_a_stretch_spans_many_requests(empties, op):
     bo = bo.astype(np.int64)
     replay([(op, (keys, bo)), ("evict", n - 1), (op, (keys, bo)), ("evict", n)],
            log2_slots=12)
+
+
+@pytest.mark.parametrize("keep", ["all", "all_but_one", "tracked_only"])
+def test_untracked_keys_in_a_sparse_table(keep):
+    """Keys inserted while tracking is off (recency word 0) form the lowest
+    rank class.  In a sparse table most waves of the rank gather hold only
+    untracked keys or only tracked ones, and the untracked class must still
+    enter the select: evict(count) keeps every key, evict(count - 1) drops
+    exactly the untracked class (it no longer fits whole)."""
+    untracked = arr([key_of(1000 + i) for i in range(3)])
+    tracked = arr([key_of(2000 + i) for i in range(5)])
+    bo = np.array([0, 5], np.int64)
+    T = O.Table()
+    T.keys |= {untracked[i].tobytes() for i in range(3)}  # no recency recorded
+    T.insert(tracked, bo)
+    max_keys = {"all": 8, "all_but_one": 7, "tracked_only": 5}[keep]
+    with KV.Cache(16) as c:
+        c.insert(dev(untracked), dev(np.array([0, 3], np.int64)))
+        c.set_recency(True)
+        c.insert(dev(tracked), dev(bo))
+        assert c.count() == 8
+        assert c.evict(max_keys) == T.evict(max_keys)
+        assert key_set(c.export()) == T.keys
+    assert len(T.keys) == (8 if keep == "all" else 5)
