@@ -41,9 +41,6 @@
 #include "common.h"
 #include "sha256_cdna4.h"
 
-#ifndef KVGOV_LANE_PAIR
-#define KVGOV_LANE_PAIR 1  // 0: the single-wave kernel for every batch
-#endif
 #ifndef KVGOV_LP_COVER
 #define KVGOV_LP_COVER 2  // lane-pair kernel: steps between a barrier and its first word
 #endif
@@ -561,11 +558,6 @@ __device__ __forceinline__ void single_chain(const ChainArgs &a, int32_t i) {
     take_block(nxt, T, q.tp, j + 1 < nf ? j + 1 : j, nf);
     store_digest(q.out + j * 32, H);
   }
-}
-
-template <int MODE>
-__global__ __launch_bounds__(256) void k_chains(ChainArgs a) {
-  single_chain<MODE>(a, blockIdx.x * blockDim.x + threadIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -1296,7 +1288,7 @@ static size_t lp_lds_reserve(int per_cu) {
 // batches); larger batches keep every SIMD busy with the single-wave kernel
 // (0).
 static int lp_slots(int32_t n) {
-  if (!KVGOV_LANE_PAIR || n <= 0) return 0;
+  if (n <= 0) return 0;
   const int64_t groups = ceil_div(n, (int64_t)kWave);
   const int64_t cus = device_cu_count();
   if (groups <= cus) return 1;
@@ -1402,12 +1394,22 @@ int kvgov_resume_offsets(const int64_t *tok_offsets, const int32_t *start_block,
   return block_offsets_impl(tok_offsets, start_block, n, block_size, blk_offsets, status, stream);
 }
 
-// Longest-first ordering pays once the batch has about as many waves as the
-// chip has SIMDs; below that every wave has a SIMD of its own from the start
-// and the kernel takes as long as its longest chain in any order.  (Batches
-// that run on the lane-pair kernel are resident all at once and are never
-// ordered.)
-static int64_t order_min_requests() { return (int64_t)device_cu_count() * 4 * kWave / 2; }
+// Longest-first order of a batch's requests (counting sort of their block
+// counts) in `scratch`: kOrderBuckets + n int32 (the histogram, then the
+// order).  Returns the order.
+static const int32_t *order_requests(const int64_t *blk_offsets, int32_t n, int32_t *scratch,
+                                     hipStream_t s) {
+  int32_t *hist = scratch;
+  int32_t *order = scratch + kOrderBuckets;
+  hipLaunchKernelGGL(k_fill_i32, dim3(kOrderBuckets / 256), dim3(256), 0, s, hist,
+                     (int64_t)kOrderBuckets, 0);
+  const dim3 tiles((unsigned)ceil_div(n, kOrderTile));
+  hipLaunchKernelGGL(k_order_hist, tiles, dim3(kOrderThreads), 0, s, blk_offsets, n, hist);
+  hipLaunchKernelGGL(k_order_scan, dim3(1), dim3(256), 0, s, hist);
+  hipLaunchKernelGGL(k_order_scatter, tiles, dim3(kOrderThreads), 0, s, blk_offsets, n, hist,
+                     order);
+  return order;
+}
 
 static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_offsets,
                             int32_t n, const int32_t *principal, const uint8_t *salts, int32_t P,
@@ -1444,31 +1446,17 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
   a.start = start;
   a.parents = parents;
 
-  const int slots = lp_slots(n);
-  int32_t *scratch = nullptr;
-  if (!slots && n >= order_min_requests()) {
-    const size_t bytes = sizeof(int32_t) * ((size_t)kOrderBuckets + (size_t)n);
-    if (hipMallocAsync(reinterpret_cast<void **>(&scratch), bytes, s) != hipSuccess)
-      return KVGOV_E_NOMEM;
-    int32_t *hist = scratch;
-    int32_t *order = scratch + kOrderBuckets;
-    hipLaunchKernelGGL(k_fill_i32, dim3(kOrderBuckets / 256), dim3(256), 0, s, hist,
-                       (int64_t)kOrderBuckets, 0);
-    const dim3 tiles((unsigned)ceil_div(n, kOrderTile));
-    hipLaunchKernelGGL(k_order_hist, tiles, dim3(kOrderThreads), 0, s, blk_offsets, n, hist);
-    hipLaunchKernelGGL(k_order_scan, dim3(1), dim3(256), 0, s, hist);
-    hipLaunchKernelGGL(k_order_scatter, tiles, dim3(kOrderThreads), 0, s, blk_offsets, n, hist,
-                       order);
-    a.order = order;
-  }
   // Launch shape.  A chain wave is bound by its SIMD's issue rate, so it
   // should never share a SIMD while others sit idle.  The dispatcher stacks
   // the waves of concurrent launches on the same SIMDs, and the older wave
   // then takes nearly every issue slot, so the workgroups reserve LDS (unused
   // beyond the kernel's own) to bound how many share a CU.
+  const int slots = lp_slots(n);
+  int32_t *scratch = nullptr;
   if (slots) {
     // lane pairs: two rounds waves and a schedule wave per 64 requests, one
-    // or two workgroups per CU
+    // or two workgroups per CU; every request of the batch is resident from
+    // the start, so the order of the requests does not matter
     const dim3 grid((unsigned)ceil_div(n, kWave)), block(kLpThreads);
     const size_t lds = lp_lds_reserve(slots);
     switch (mode) {
@@ -1476,9 +1464,16 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
       case KVGOV_ROOT: hipLaunchKernelGGL(k_chains_lp<KVGOV_ROOT>, grid, block, lds, s, a); break;
       default: hipLaunchKernelGGL(k_chains_lp<KVGOV_BOUNDARY>, grid, block, lds, s, a); break;
     }
-  } else if (a.order && KVGOV_LANE_PAIR) {
-    // ordered batch: the longest requests on lane-pair workgroups (one
-    // eighth of the CUs), the rest one lane per request; one workgroup per CU
+  } else {
+    // More than two lane-pair workgroups per CU: the batch has at least as
+    // many waves (one lane per request) as the chip has SIMDs, and it is
+    // ordered longest first (counting sort of block counts).  The longest
+    // requests then run on lane-pair workgroups (one eighth of the CUs), the
+    // rest one lane per request; one workgroup per CU.
+    const size_t bytes = sizeof(int32_t) * ((size_t)kOrderBuckets + (size_t)n);
+    if (hipMallocAsync(reinterpret_cast<void **>(&scratch), bytes, s) != hipSuccess)
+      return KVGOV_E_NOMEM;
+    a.order = order_requests(blk_offsets, n, scratch, s);
     const int32_t lp_groups = std::max(1, device_cu_count() / 8);
     const int64_t rest = std::max<int64_t>(0, (int64_t)n - (int64_t)lp_groups * kWave);
     const dim3 grid((unsigned)(lp_groups + ceil_div(rest, 4 * kWave))), block(4 * kWave);
@@ -1488,17 +1483,6 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
       case KVGOV_NONE: hipLaunchKernelGGL(k_chains_mixed<KVGOV_NONE>, grid, block, lds, s, a, lp_groups); break;
       case KVGOV_ROOT: hipLaunchKernelGGL(k_chains_mixed<KVGOV_ROOT>, grid, block, lds, s, a, lp_groups); break;
       default: hipLaunchKernelGGL(k_chains_mixed<KVGOV_BOUNDARY>, grid, block, lds, s, a, lp_groups); break;
-    }
-  } else {
-    // at most one workgroup per CU; batches of at most one wave per CU run
-    // one wave per workgroup, larger ones four (one per SIMD)
-    const int threads = (int64_t)n <= (int64_t)device_cu_count() * kWave ? kWave : 4 * kWave;
-    const dim3 grid((unsigned)ceil_div(n, threads)), block(threads);
-    const size_t lds = chain_lds_reserve();
-    switch (mode) {
-      case KVGOV_NONE: hipLaunchKernelGGL(k_chains<KVGOV_NONE>, grid, block, lds, s, a); break;
-      case KVGOV_ROOT: hipLaunchKernelGGL(k_chains<KVGOV_ROOT>, grid, block, lds, s, a); break;
-      default: hipLaunchKernelGGL(k_chains<KVGOV_BOUNDARY>, grid, block, lds, s, a); break;
     }
   }
   int rc = launch_status();
