@@ -77,6 +77,10 @@ extern "C" {
 #define KVGOV_E_CAPACITY (-9)    /* export buffer smaller than the key count */
 #define KVGOV_E_DEVICE (-10)     /* cache used with another device current */
 #define KVGOV_E_INTERNAL (-11)   /* kernel: a bounded wait ran out (never expected) */
+#define KVGOV_E_TOO_LARGE (-12)  /* batch above the allocation-free entry point's limit */
+
+/* Largest batch (requests) of kvgov_hash_chains_noalloc. */
+#define KVGOV_NOALLOC_MAX_REQUESTS 2097152
 
 /* Opaque, library-owned prefix-cache table on one device. */
 typedef struct kvgov_cache kvgov_cache;
@@ -137,8 +141,9 @@ int kvgov_block_offsets(const int64_t *tok_offsets, int32_t n, int32_t block_siz
  * status       device int32, zeroed by the caller; kernels store the first
  *              error (KVGOV_E_OFFSETS / _PRINCIPAL / _BOUNDARY) there and skip
  *              the offending request.
- * Scratch: for large batches the call orders requests longest first using
- * 8 * n bytes from hipMallocAsync on `stream`, freed in stream order.
+ * Scratch: batches of more than two 64-request lane-pair workgroups per CU
+ * (n > 128 * CUs) are ordered longest first using 4 * (4096 + n) bytes from
+ * hipMallocAsync on `stream`, freed in stream order.
  * Errors: KVGOV_E_INVAL, KVGOV_E_UNSUPPORTED, KVGOV_E_NOMEM, KVGOV_E_HIP.
  */
 int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens,
@@ -147,6 +152,30 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens,
                       int32_t mode, const int32_t *boundary_tok, int32_t block_size,
                       const int64_t *blk_offsets, uint8_t *hashes, int64_t n_blocks,
                       int32_t *status, void *stream);
+
+/*
+ * kvgov_hash_chains for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, results and errors as kvgov_hash_chains; it
+ * calls no hipMalloc, hipFree or allocating library routine.  The ordering
+ * scratch of large batches is a fixed array inside the library, one per
+ * device (4 * (4096 + KVGOV_NOALLOC_MAX_REQUESTS) bytes, about 8 MiB, held
+ * until the process ends; its address is looked up on the first call on
+ * each device).  Every call on a device shares that device's array, so
+ * calls that overlap on one device (on different streams, or from several
+ * host threads, without ordering between them) race and must not be
+ * issued; calls in one stream are ordered and safe.  The histogram part is
+ * cleared by a kernel at the start of each call.
+ * Errors: as kvgov_hash_chains, and KVGOV_E_TOO_LARGE (before anything else
+ * is checked) for n > KVGOV_NOALLOC_MAX_REQUESTS; KVGOV_E_HIP if the
+ * scratch's address cannot be obtained.
+ */
+int kvgov_hash_chains_noalloc(const int32_t *tokens, int64_t n_tokens,
+                              const int64_t *tok_offsets, int32_t n,
+                              const int32_t *principal, const uint8_t *salts, int32_t P,
+                              int32_t mode, const int32_t *boundary_tok, int32_t block_size,
+                              const int64_t *blk_offsets, uint8_t *hashes, int64_t n_blocks,
+                              int32_t *status, void *stream);
 
 /*
  * Chain extension (Sec. 2.1; Sec. 5.7 on multi-turn sessions, where turn

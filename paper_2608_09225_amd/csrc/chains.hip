@@ -1313,6 +1313,38 @@ int device_cu_count() {
   return cus[dev];
 }
 
+// Scratch of the allocation-free hashing entry point: the longest-first
+// order of a batch (histogram, then the order), kOrderBuckets + n int32 for
+// n up to KVGOV_NOALLOC_MAX_REQUESTS.  One copy per device, held until the
+// process ends; host code reaches it only through the address that
+// hipGetSymbolAddress returns on that device (the array's name is a host
+// stand-in, not a device address).
+constexpr int64_t kNoAllocScratchInts = (int64_t)kOrderBuckets + KVGOV_NOALLOC_MAX_REQUESTS;
+static __device__ __align__(256) int32_t scratch[kNoAllocScratchInts];
+
+// Device address of `scratch` on the current device, looked up once per
+// device; NULL if the lookup fails.
+static int32_t *noalloc_scratch() {
+  static std::mutex mu;
+  static std::vector<int32_t *> ptrs;
+  static std::vector<char> looked_up;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return nullptr;
+  std::lock_guard<std::mutex> g(mu);
+  if ((int)ptrs.size() <= dev) {
+    ptrs.resize(dev + 1, nullptr);
+    looked_up.resize(dev + 1, 0);
+  }
+  if (!looked_up[dev]) {
+    int32_t *ptr = nullptr;
+    if (hipGetSymbolAddress(reinterpret_cast<void **>(&ptr), HIP_SYMBOL(scratch)) != hipSuccess)
+      return nullptr;  // not cached: a later call tries again
+    ptrs[dev] = ptr;
+    looked_up[dev] = 1;
+  }
+  return ptrs[dev];
+}
+
 }  // namespace kvgov
 
 using namespace kvgov;
@@ -1333,6 +1365,8 @@ const char *kvgov_strerror(int code) {
     case KVGOV_E_CAPACITY: return "export buffer too small";
     case KVGOV_E_DEVICE: return "cache used with a different current device";
     case KVGOV_E_INTERNAL: return "bounded wait exhausted inside a kernel";
+    case KVGOV_E_TOO_LARGE:
+      return "batch above KVGOV_NOALLOC_MAX_REQUESTS requests (allocation-free entry point)";
     default: return "unknown error code";
   }
 }
@@ -1395,12 +1429,12 @@ int kvgov_resume_offsets(const int64_t *tok_offsets, const int32_t *start_block,
 }
 
 // Longest-first order of a batch's requests (counting sort of their block
-// counts) in `scratch`: kOrderBuckets + n int32 (the histogram, then the
+// counts) in `buf`: kOrderBuckets + n int32 (the histogram, then the
 // order).  Returns the order.
-static const int32_t *order_requests(const int64_t *blk_offsets, int32_t n, int32_t *scratch,
+static const int32_t *order_requests(const int64_t *blk_offsets, int32_t n, int32_t *buf,
                                      hipStream_t s) {
-  int32_t *hist = scratch;
-  int32_t *order = scratch + kOrderBuckets;
+  int32_t *hist = buf;
+  int32_t *order = buf + kOrderBuckets;
   hipLaunchKernelGGL(k_fill_i32, dim3(kOrderBuckets / 256), dim3(256), 0, s, hist,
                      (int64_t)kOrderBuckets, 0);
   const dim3 tiles((unsigned)ceil_div(n, kOrderTile));
@@ -1416,7 +1450,7 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
                             int32_t mode, const int32_t *boundary_tok, int32_t block_size,
                             const int32_t *start, const uint8_t *parents,
                             const int64_t *blk_offsets, uint8_t *hashes, int64_t n_blocks,
-                            int32_t *status, void *stream) {
+                            int32_t *status, void *stream, bool noalloc) {
   if (n < 0 || n_tokens < 0 || n_blocks < 0 || !status) return KVGOV_E_INVAL;
   if (mode != KVGOV_NONE && mode != KVGOV_ROOT && mode != KVGOV_BOUNDARY) return KVGOV_E_INVAL;
   if (block_size != KVGOV_BLOCK_SIZE) return KVGOV_E_UNSUPPORTED;
@@ -1452,7 +1486,7 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
   // then takes nearly every issue slot, so the workgroups reserve LDS (unused
   // beyond the kernel's own) to bound how many share a CU.
   const int slots = lp_slots(n);
-  int32_t *scratch = nullptr;
+  int32_t *owned = nullptr;  // stream-ordered scratch of this call
   if (slots) {
     // lane pairs: two rounds waves and a schedule wave per 64 requests, one
     // or two workgroups per CU; every request of the batch is resident from
@@ -1470,10 +1504,19 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
     // ordered longest first (counting sort of block counts).  The longest
     // requests then run on lane-pair workgroups (one eighth of the CUs), the
     // rest one lane per request; one workgroup per CU.
-    const size_t bytes = sizeof(int32_t) * ((size_t)kOrderBuckets + (size_t)n);
-    if (hipMallocAsync(reinterpret_cast<void **>(&scratch), bytes, s) != hipSuccess)
-      return KVGOV_E_NOMEM;
-    a.order = order_requests(blk_offsets, n, scratch, s);
+    // The ordering scratch: the library's fixed array for the
+    // allocation-free entry point, else stream-ordered.
+    int32_t *buf = nullptr;
+    if (noalloc) {
+      buf = noalloc_scratch();
+      if (!buf) return KVGOV_E_HIP;
+    } else {
+      const size_t bytes = sizeof(int32_t) * ((size_t)kOrderBuckets + (size_t)n);
+      if (hipMallocAsync(reinterpret_cast<void **>(&owned), bytes, s) != hipSuccess)
+        return KVGOV_E_NOMEM;
+      buf = owned;
+    }
+    a.order = order_requests(blk_offsets, n, buf, s);
     const int32_t lp_groups = std::max(1, device_cu_count() / 8);
     const int64_t rest = std::max<int64_t>(0, (int64_t)n - (int64_t)lp_groups * kWave);
     const dim3 grid((unsigned)(lp_groups + ceil_div(rest, 4 * kWave))), block(4 * kWave);
@@ -1486,7 +1529,7 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
     }
   }
   int rc = launch_status();
-  if (scratch && hipFreeAsync(scratch, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
+  if (owned && hipFreeAsync(owned, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
   return rc;
 }
 
@@ -1497,7 +1540,19 @@ int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *to
                       int32_t *status, void *stream) {
   return hash_chains_impl(tokens, n_tokens, tok_offsets, n, principal, salts, P, mode,
                           boundary_tok, block_size, nullptr, nullptr, blk_offsets, hashes,
-                          n_blocks, status, stream);
+                          n_blocks, status, stream, false);
+}
+
+int kvgov_hash_chains_noalloc(const int32_t *tokens, int64_t n_tokens,
+                              const int64_t *tok_offsets, int32_t n, const int32_t *principal,
+                              const uint8_t *salts, int32_t P, int32_t mode,
+                              const int32_t *boundary_tok, int32_t block_size,
+                              const int64_t *blk_offsets, uint8_t *hashes, int64_t n_blocks,
+                              int32_t *status, void *stream) {
+  if (n > KVGOV_NOALLOC_MAX_REQUESTS) return KVGOV_E_TOO_LARGE;
+  return hash_chains_impl(tokens, n_tokens, tok_offsets, n, principal, salts, P, mode,
+                          boundary_tok, block_size, nullptr, nullptr, blk_offsets, hashes,
+                          n_blocks, status, stream, true);
 }
 
 int kvgov_hash_chains_resume(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_offsets,
@@ -1510,7 +1565,7 @@ int kvgov_hash_chains_resume(const int32_t *tokens, int64_t n_tokens, const int6
   if (reinterpret_cast<uintptr_t>(parents) & 3) return KVGOV_E_INVAL;
   return hash_chains_impl(tokens, n_tokens, tok_offsets, n, principal, salts, P, mode,
                           boundary_tok, block_size, start_block, parents, blk_offsets, hashes,
-                          n_blocks, status, stream);
+                          n_blocks, status, stream, false);
 }
 
 }  // extern "C"

@@ -11,6 +11,7 @@ Calls mirror the C ABI one to one:
     kvgov_salts         -> salts(K, principal_ids)
     kvgov_block_offsets -> block_offsets(tok_offsets)
     kvgov_hash_chains   -> hash_chains(tokens, tok_offsets, principal, salts, mode, ...)
+    kvgov_hash_chains_noalloc -> hash_chains_noalloc(..., blk_offsets, out, status)
     kvgov_hash_chains_resume -> hash_chains_resume(..., start_block, parents, ...)
     kvgov_resume_offsets -> resume_offsets(tok_offsets, start_block)
     kvgov_cache_*       -> Cache(log2_slots).insert / lookup / admit / set_recency / evict /
@@ -43,6 +44,9 @@ _SIGNATURES = {
     "kvgov_block_offsets": (ctypes.c_int, [_vp, _c_i32, _c_i32, _vp, _vp, _vp]),
     "kvgov_hash_chains": (ctypes.c_int, [_vp, _c_i64, _vp, _c_i32, _vp, _vp, _c_i32, _c_i32,
                                          _vp, _c_i32, _vp, _vp, _c_i64, _vp, _vp]),
+    "kvgov_hash_chains_noalloc": (ctypes.c_int, [_vp, _c_i64, _vp, _c_i32, _vp, _vp, _c_i32,
+                                                 _c_i32, _vp, _c_i32, _vp, _vp, _c_i64, _vp,
+                                                 _vp]),
     "kvgov_hash_chains_resume": (ctypes.c_int, [_vp, _c_i64, _vp, _c_i32, _vp, _vp, _c_i32,
                                                 _c_i32, _vp, _c_i32, _vp, _vp, _vp, _vp,
                                                 _c_i64, _vp, _vp]),
@@ -225,6 +229,33 @@ def hash_chains(tokens: torch.Tensor, tok_offsets: torch.Tensor, principal: Opti
                                    _stream(stream)), "kvgov_hash_chains")
     if check:
         check_status(status, "kvgov_hash_chains")
+    return out
+
+
+def hash_chains_noalloc(tokens: torch.Tensor, tok_offsets: torch.Tensor,
+                        principal: Optional[torch.Tensor], salt_table: Optional[torch.Tensor],
+                        mode: int, boundary_tok: Optional[torch.Tensor],
+                        blk_offsets: torch.Tensor, out: torch.Tensor, status: torch.Tensor,
+                        stream=None) -> torch.Tensor:
+    """kvgov_hash_chains_noalloc: as hash_chains, with every buffer given by
+    the caller (block offsets, output rows, status word), so that neither
+    the library nor this binding allocates device memory.  Does not wait:
+    errors the kernels find stay latched in ``status``."""
+    tk = _dev(tokens, torch.int32, "tokens")
+    to = _dev(tok_offsets, torch.int64, "tok_offsets")
+    n = to.numel() - 1
+    pr = _dev(principal, torch.int32, "principal", allow_none=(mode == NONE))
+    st = _dev(salt_table, torch.uint8, "salts", allow_none=(mode == NONE))
+    bt = _dev(boundary_tok, torch.int32, "boundary_tok", allow_none=(mode != BOUNDARY))
+    bo = _dev(blk_offsets, torch.int64, "blk_offsets")
+    _dev(out, torch.uint8, "out")
+    _dev(status, torch.int32, "status")
+    P = 0 if st is None else int(st.shape[0])
+    _check(lib().kvgov_hash_chains_noalloc(_ptr(tk), tk.numel(), _ptr(to), n, _ptr(pr),
+                                           _ptr(st), P, int(mode), _ptr(bt), BLOCK, _ptr(bo),
+                                           _ptr(out), out.shape[0] if out.dim() else 0,
+                                           _ptr(status), _stream(stream)),
+           "kvgov_hash_chains_noalloc")
     return out
 
 

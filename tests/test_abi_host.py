@@ -74,6 +74,23 @@ def test_host_validation_returns_before_any_launch():
         a.update(kw)
         return L.kvgov_hash_chains(*a.values())
 
+    def chains_noalloc(**kw):
+        a = dict(tokens=fake, n_tokens=64, tok_offsets=fake, n=2, principal=fake, salts=fake,
+                 P=4, mode=K.ROOT, boundary_tok=fake, block_size=16, blk_offsets=fake,
+                 hashes=fake, n_blocks=4, status=fake, stream=None)
+        a.update(kw)
+        return L.kvgov_hash_chains_noalloc(*a.values())
+
+    # the allocation-free variant: the size limit first, then the same checks
+    big = c["KVGOV_NOALLOC_MAX_REQUESTS"] + 1
+    assert chains_noalloc(n=big, tokens=None, status=None) == c["KVGOV_E_TOO_LARGE"]
+    assert chains_noalloc(n=-1) == INVAL
+    assert chains_noalloc(mode=3) == INVAL
+    assert chains_noalloc(block_size=32) == UNSUP
+    assert chains_noalloc(status=None) == INVAL
+    assert chains_noalloc(tok_offsets=None) == INVAL
+    assert chains_noalloc(n=0, tokens=None, hashes=None) == 0  # nothing to do
+
     assert chains(n=-1) == INVAL
     assert chains(mode=3) == INVAL
     assert chains(block_size=32) == UNSUP
