@@ -303,9 +303,10 @@ __device__ __forceinline__ int order_bucket(const int64_t *blk_offsets, int32_t 
 // Histogram and scatter work on tiles of kOrderTile requests per workgroup and
 // count in LDS first, so global atomics are one per (tile, non-empty bucket):
 // per-request atomics on a few hot bucket counters serialise (4 ms for a
-// 1.25M-request batch).
-constexpr int kOrderThreads = 1024;
-constexpr int kOrderPerThread = 4;
+// 1.25M-request batch).  Workgroups of four waves find room on a busy chip
+// (other streams' kernels in flight) far sooner than workgroups of sixteen.
+constexpr int kOrderThreads = 256;
+constexpr int kOrderPerThread = 16;
 constexpr int64_t kOrderTile = (int64_t)kOrderThreads * kOrderPerThread;
 
 __global__ __launch_bounds__(kOrderThreads) void k_order_hist(const int64_t *blk_offsets,
