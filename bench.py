@@ -263,6 +263,20 @@ def admit_group(n: int, rows: int) -> int:
     return g
 
 
+def lookup_lanes(n: int, n_blocks: int) -> int:
+    """Lanes per request of the lookup kernel (the library's rule)."""
+    g = 1
+    while g < 64 and n * g * 2 <= (1 << 18):
+        g <<= 1
+    avg = n_blocks // n if n else 0
+    while g < 64 and g * 16 <= avg and n * g * 2 <= (1 << 21):
+        g <<= 1
+    if avg >= 128:
+        while g < 64 and n * g * 2 <= (1 << 22):
+            g <<= 1
+    return g
+
+
 def lookup_bytes(counts: np.ndarray, hits: np.ndarray) -> int:
     examined = np.minimum(hits.astype(np.int64) + 1, counts)
     return int(examined.sum()) * LOOKUP_BYTES_PER_BLOCK + counts.size * LOOKUP_BYTES_PER_REQUEST
@@ -1092,12 +1106,7 @@ def run_workload(name: str, args, dev, K, torch):
         look_bytes = {m: lookup_bytes(cntB, got_hits[m]) for m in modes}
     look_mean = {m: float(np.mean(ts)) for m, ts in look_t.items()}
     look_gbs = float(np.mean([look_bytes[m] / look_mean[m] for m in modes])) / 1e9
-    g_look = 1  # lanes per request the library picks for this batch
-    while g_look < 64 and B.n * g_look * 2 <= (1 << 18):
-        g_look <<= 1
-    avg_blocks = int(cntB.sum()) // max(B.n, 1)
-    while g_look < 64 and g_look * 16 <= avg_blocks and B.n * g_look * 2 <= (1 << 21):
-        g_look <<= 1
+    g_look = lookup_lanes(B.n, int(cntB.sum()))
     ltr = recorded_traffic(f"k_lookup<{g_look}>", wl.name, "cache")
     roof_lookup = {
         "bound": "hbm", "kernel": "k_lookup (first-miss prefix lookup)",
@@ -1470,8 +1479,8 @@ def run_workload(name: str, args, dev, K, torch):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default=HEADLINE, choices=sorted(DESCRIPTIONS),
                     help=f"workload of the bench line (default {HEADLINE}; with the default, "
                          f"the other configs {', '.join(SECONDARY)} are timed after it and "

@@ -202,7 +202,11 @@ struct LookupArgs {
 
 // G lanes per request take G consecutive blocks at a time; a ballot over the
 // group finds the first miss, and the group stops at the first chunk that
-// holds one.
+// holds one.  A probe reads its key's bucket (one 128-byte line) at once:
+// loads of single slots, the later ones hitting the line in the cache, and
+// several probes in flight per lane (over blocks past the first miss) both
+// measured slower on the probe-heavy workload, whose lookup is bound by the
+// lines it moves.
 template <int G>
 __global__ __launch_bounds__(256) void k_lookup(LookupArgs a) {
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -223,42 +227,14 @@ __global__ __launch_bounds__(256) void k_lookup(LookupArgs a) {
   const bool ones = a.t.meta->ones_present != 0;
   const int64_t nf = b1 - b0;
   int64_t hit = nf;
-  if constexpr (G == 1) {
-    // One lane per request: its query keys are read a 128-byte line (four
-    // keys) at a time, so each line of the hashes array is fetched once
-    // instead of once per key.
-    int64_t j = 0;
-    bool stop = false;
-    while (!stop && j < nf) {
-      const int64_t idx = b0 + j;
-      const int64_t line = idx & ~(int64_t)3;
-      Key q[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        q[u] = (line + u < a.n_blocks) ? load_key(a.hashes + (line + u) * 32) : Key{};
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        if (!stop && line + u >= idx && j < nf) {
-          if (probe(a.t, q[u], ones)) {
-            ++j;
-          } else {
-            hit = j;
-            stop = true;
-          }
-        }
-      }
-    }
-  } else {
-    for (int64_t j0 = 0; j0 < nf; j0 += G) {
-      const int64_t j = j0 + sub;
-      bool miss = false;
-      if (j < nf) miss = !probe(a.t, load_key(a.hashes + (b0 + j) * 32), ones);
-      const uint64_t m = __ballot(miss) & gmask;
-      if (m) {
-        hit = j0 + (__builtin_ctzll(m) - base);
-        break;
-      }
+  for (int64_t j0 = 0; j0 < nf; j0 += G) {
+    const int64_t j = j0 + sub;
+    bool miss = false;
+    if (j < nf) miss = !probe(a.t, load_key(a.hashes + (b0 + j) * 32), ones);
+    const uint64_t m = __ballot(miss) & gmask;
+    if (m) {
+      hit = j0 + (__builtin_ctzll(m) - base);
+      break;
     }
   }
   if (sub == 0) a.hit_blocks[r] = (int32_t)hit;
@@ -710,6 +686,31 @@ __global__ __launch_bounds__(256) void k_reinsert(TableView t, const SelectState
     atomicAdd(&t.meta->n_keys[blockIdx.x % kCounterLanes], (unsigned long long)total);
 }
 
+// Lanes per request for lookup: enough groups in flight to cover the chip
+// (about 2^18 lanes), one lane each when the batch alone is that large; and,
+// up to about 2^21 lanes, one lane per ~16 blocks of the average request,
+// since a group walks its request's blocks G at a time and the longest
+// request bounds the launch (a batch of long requests would otherwise wait on
+// its longest one with one or two lanes).
+//
+// Batches of long requests (128 blocks or more on average) go to a full wave
+// per request, up to 2^22 lanes: the launch then ends when the longest
+// request's last round does, and a request of L blocks takes L / G rounds
+// (65,536 requests averaging 208 blocks, at most 2048: 1.65 / 1.00 ms per
+// lookup with 16 lanes per request, 1.34 / 0.75 ms with 64).  Short
+// requests keep fewer lanes: their probes stop at the first miss, and spare
+// lanes would only probe past it (1M probes of 8..64 blocks: 0.43 ms with 2
+// lanes, 0.45 ms with 4).
+static int lookup_group(int32_t n, int64_t n_blocks) {
+  int g = 1;
+  while (g < 64 && (int64_t)n * g * 2 <= (1 << 18)) g <<= 1;
+  const int64_t avg = n > 0 ? n_blocks / n : 0;
+  while (g < 64 && (int64_t)g * 16 <= avg && (int64_t)n * g * 2 <= (1 << 21)) g <<= 1;
+  if (avg >= 128)
+    while (g < 64 && (int64_t)n * g * 2 <= (1 << 22)) g <<= 1;
+  return g;
+}
+
 }  // namespace kvgov
 
 using namespace kvgov;
@@ -913,20 +914,6 @@ int kvgov_cache_insert(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
   rc = cache_insert_rows(c, hashes, blk_offsets, n, n_blocks, s, &epoch);
   if (rc != KVGOV_OK || !n_new) return rc;
   return read_new_keys(c, epoch, n_new, s);
-}
-
-// Lanes per request for lookup: enough groups in flight to cover the chip
-// (about 2^18 lanes), one lane each when the batch alone is that large; and,
-// up to about 2^21 lanes, one lane per ~16 blocks of the average request,
-// since a group walks its request's blocks G at a time and the longest
-// request bounds the launch (a batch of long requests would otherwise wait on
-// its longest one with one or two lanes).
-static int lookup_group(int32_t n, int64_t n_blocks) {
-  int g = 1;
-  while (g < 64 && (int64_t)n * g * 2 <= (1 << 18)) g <<= 1;
-  const int64_t avg = n > 0 ? n_blocks / n : 0;
-  while (g < 64 && (int64_t)g * 16 <= avg && (int64_t)n * g * 2 <= (1 << 21)) g <<= 1;
-  return g;
 }
 
 int kvgov_cache_lookup(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_offsets,

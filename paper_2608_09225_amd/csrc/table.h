@@ -79,6 +79,19 @@ __device__ __forceinline__ uint64_t slot_hash(const Key &k) {
   return x;
 }
 
+// A key's probe sequence starts at the first slot of a 4-slot bucket: the
+// bucket's keys fill one 128-byte line, so a probe of a present key reads
+// one line unless its bucket has overflowed (four slots hold the keys that
+// hash to a bucket, at half load mostly), where linear probing from an
+// arbitrary slot reads two lines whenever the sequence crosses a line end.
+// The sequence then runs through the following slots as plain linear
+// probing does.
+constexpr uint64_t kBucketSlots = 4;
+
+__device__ __forceinline__ uint64_t home_slot(const Key &k, uint64_t mask) {
+  return slot_hash(k) & mask & ~(kBucketSlots - 1);
+}
+
 // Sum of v over the workgroup (256 threads), valid in thread 0.
 __device__ __forceinline__ uint32_t block_sum(uint32_t v, uint32_t *lds4) {
 #pragma unroll
@@ -146,7 +159,7 @@ __device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &ke
     if (t.track && depth != kNoDepth) touch(&t.meta->ones_rank, recency(epoch, depth), won);
     return won ? 1u : 0u;
   }
-  uint64_t s = slot_hash(key) & t.mask;
+  uint64_t s = home_slot(key, t.mask);
   for (uint64_t probes = 0; probes <= t.mask; ++probes) {
     unsigned long long tag = t.tags[s];
     if (tag == 0) {
@@ -182,15 +195,21 @@ __device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &ke
   return 0;
 }
 
-// Is `key` in the table?  Reads the key array only.
+// Is `key` in the table?  Reads the key array only, a bucket (one 128-byte
+// line) per memory round trip; the slots are then examined in probe order.
 __device__ __forceinline__ bool probe(const TableView &t, const Key &key, bool ones_present) {
   if (key_is_empty_pattern(key)) return ones_present;
-  uint64_t s = slot_hash(key) & t.mask;
-  for (uint64_t p = 0; p <= t.mask; ++p) {
-    const Key slot{t.keys[2 * s], t.keys[2 * s + 1]};
-    if (key_eq(slot, key)) return true;
-    if (key_is_empty_pattern(slot)) return false;
-    s = (s + 1) & t.mask;
+  uint64_t s = home_slot(key, t.mask);
+  for (uint64_t p = 0; p <= t.mask; p += kBucketSlots) {
+    Key b[kBucketSlots];
+#pragma unroll
+    for (uint64_t u = 0; u < kBucketSlots; ++u) b[u] = Key{t.keys[2 * (s + u)], t.keys[2 * (s + u) + 1]};
+#pragma unroll
+    for (uint64_t u = 0; u < kBucketSlots; ++u) {
+      if (key_eq(b[u], key)) return true;
+      if (key_is_empty_pattern(b[u])) return false;
+    }
+    s = (s + kBucketSlots) & t.mask;
   }
   return false;
 }
@@ -208,7 +227,7 @@ __device__ __forceinline__ uint64_t group_mask(int base) {
 // Slot holding `key`, or -1 (the all-0xFF key has no slot: -2 if present).
 __device__ __forceinline__ int64_t find_slot(const TableView &t, const Key &key) {
   if (key_is_empty_pattern(key)) return t.meta->ones_present ? -2 : -1;
-  uint64_t s = slot_hash(key) & t.mask;
+  uint64_t s = home_slot(key, t.mask);
   for (uint64_t p = 0; p <= t.mask; ++p) {
     const Key slot{t.keys[2 * s], t.keys[2 * s + 1]};
     if (key_eq(slot, key)) return (int64_t)s;
