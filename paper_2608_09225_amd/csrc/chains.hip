@@ -964,6 +964,65 @@ __device__ __forceinline__ void lp_round_groups(uint32_t s[4], uint32_t &z, uint
   }
 }
 
+// Message schedule on a lane pair: with two schedule lanes per request,
+// lane p of the pair makes the words W[t], t = 16 + 2k + p, of step k, so a
+// wave makes a word of 32 requests in about 16 instructions per two words
+// instead of one lane making every word in 11.  Both lanes keep a 16-word
+// window in which lane p's logical word i at step k is W[2k + p + i],
+// stored at w[(2k + i) & 15]: the four operands of W[t] (t - 16, t - 15,
+// t - 7, t - 2: logical 0, 1, 9, 14) are then the same registers on both
+// lanes.  After the step each lane takes its partner's new word with one DPP
+// swap: lane 0 needs it as logical 15 of the next window (W[17 + 2k]), lane 1
+// as logical 13 (W[16 + 2k]); lane 1's logical 15 (W[18 + 2k], lane 0's next
+// word) is set the same way one step later, before it is first read (as
+// logical 9, four steps on).  rows[2k + p][col] receives K[t] + W[t].
+template <int K>
+__device__ __forceinline__ void lp_pair_step(uint32_t w[16], uint32_t (*rows)[kLpCols], int col,
+                                             bool odd) {
+  constexpr int i0 = (2 * K) & 15, i1 = (2 * K + 1) & 15, i9 = (2 * K + 9) & 15;
+  constexpr int i14 = (2 * K + 14) & 15, i15 = (2 * K + 15) & 15;
+  const uint32_t v = small_sigma1(w[i14]) + w[i9] + small_sigma0(w[i1]) + w[i0];
+  const uint32_t kt = odd ? kSha.K[17 + 2 * K] : kSha.K[16 + 2 * K];
+  rows[2 * K + (odd ? 1 : 0)][col] = v + kt;
+  const uint32_t pv = lp_partner(v);
+  w[i0] = v;                    // logical 14 of the next window
+  w[i1] = pv;                   // logical 15 (lane 1: replaced before it is read)
+  w[i15] = odd ? pv : w[i15];   // logical 13 on lane 1
+}
+
+// Steps K .. K + N - 1.
+template <int K, int N>
+__device__ __forceinline__ void lp_pair_run(uint32_t w[16], uint32_t (*rows)[kLpCols], int col,
+                                            bool odd) {
+  if constexpr (N > 0) {
+    lp_pair_step<K>(w, rows, col, odd);
+    lp_pair_run<K + 1, N - 1>(w, rows, col, odd);
+  }
+}
+
+// The window of step 0 from the message words m[0..15] (all on both lanes):
+// lane 1's logical i is W[i + 1]; its logical 15 (W[16]) comes from lane 0's
+// first step.
+__device__ __forceinline__ void lp_pair_window(const uint32_t m[16], uint32_t w[16], bool odd) {
+#pragma unroll
+  for (int i = 0; i < 15; ++i) w[i] = odd ? m[i + 1] : m[i];
+  w[15] = m[15];
+}
+
+// The first compression's schedule in groups, as lp_sched_groups, on lane
+// pairs: group g's words, then the barrier that releases them.
+template <int G>
+__device__ __forceinline__ void lp_pair_groups(uint32_t w[16], uint32_t (*rows)[kLpCols], int col,
+                                               bool odd, bool work) {
+  if constexpr (G < kLpGroups) {
+    constexpr int S = kLpGroup[G], N = kLpGroup[G + 1] - kLpGroup[G];
+    static_assert(S % 2 == 0 && N % 2 == 0, "pair groups hold whole steps");
+    if (work) lp_pair_run<(S - 16) / 2, N / 2>(w, rows, col, odd);
+    __syncthreads();
+    lp_pair_groups<G + 1>(w, rows, col, odd, work);
+  }
+}
+
 // Per block and request, the three message patterns of the chain (the
 // compressions of a block, "first" and "second", plus a third for the
 // boundary block):
@@ -974,10 +1033,9 @@ __device__ __forceinline__ void lp_round_groups(uint32_t s[4], uint32_t &z, uint
 // Prepared one block ahead from tokens and constants: the first message's
 // words into ha / hb except h_{j-1} (written by the rounds lanes at the end
 // of block j - 1), and K + W of all 64 rounds of the second message.
-__device__ __forceinline__ void lp_prepare(const uint32_t Tn[16], const uint32_t sig[8],
+__device__ __forceinline__ void lp_message(const uint32_t Tn[16], const uint32_t sig[8],
                                            bool first_block, bool boundary, LpLds &L, int buf,
-                                           int lane) {
-  uint32_t m[16];
+                                           int lane, uint32_t m[16]) {
   if (boundary) {
 #pragma unroll
     for (int x = 0; x < 8; ++x) L.ha[x][lane] = sig[x];
@@ -1003,9 +1061,27 @@ __device__ __forceinline__ void lp_prepare(const uint32_t Tn[16], const uint32_t
   }
 #pragma unroll
   for (int x = 0; x < 16; ++x) L.c2[buf][x][lane] = kSha.K[x] + m[x];
+}
+
+__device__ __forceinline__ void lp_prepare(const uint32_t Tn[16], const uint32_t sig[8],
+                                           bool first_block, bool boundary, LpLds &L, int buf,
+                                           int lane) {
+  uint32_t m[16];
+  lp_message(Tn, sig, first_block, boundary, L, buf, lane, m);
   lp_sched16<16>(m, L.c2[buf], 16, lane);
   lp_sched16<32>(m, L.c2[buf], 32, lane);
   lp_sched16<48>(m, L.c2[buf], 48, lane);
+}
+
+// lp_prepare on a lane pair: both lanes write the same message words (the
+// same values to the same addresses), the schedule is split by parity.
+__device__ __forceinline__ void lp_prepare_pair(const uint32_t Tn[16], const uint32_t sig[8],
+                                                bool first_block, bool boundary, LpLds &L, int buf,
+                                                int col, bool odd) {
+  uint32_t m[16], w[16];
+  lp_message(Tn, sig, first_block, boundary, L, buf, col, m);
+  lp_pair_window(m, w, odd);
+  lp_pair_run<0, 24>(w, L.c2[buf] + 16, col, odd);
 }
 
 __device__ __forceinline__ void lp_load16(uint32_t w[16], const uint32_t (*rows)[2], int base,
@@ -1042,17 +1118,22 @@ __device__ __forceinline__ void lp_compress_rows(uint32_t st[4], const uint32_t 
 }
 
 // Workgroup `group` of the lane-pair kernel: requests group * 64 + 0..63 of
-// the (ordered) batch.  Waves 0 and 1 run the rounds, wave 2 the schedule; a
-// fourth wave (workgroups of 256 lanes) only keeps the barriers.
-template <int MODE>
+// the (ordered) batch.  Waves 0 and 1 run the rounds.  PAIR (workgroups of
+// four waves): waves 2 and 3 run the schedule with two lanes per request
+// (32 requests each), so that the first compression's words are ready before
+// the rounds take them; otherwise wave 2 runs it with one lane per request
+// (and a fourth wave, if any, only keeps the barriers).
+template <int MODE, bool PAIR>
 __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLds &L) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const bool sched_wave = wave >= 2;
-  const bool idle = wave >= 3;
+  const bool idle = !PAIR && wave >= 3;
   const bool a_lane = !sched_wave && (lane & 1);
+  // the lane's parity in a schedule pair
+  const bool odd = PAIR && sched_wave && (lane & 1);
   // the request (LDS column) of this lane within the workgroup
-  const int mine = sched_wave ? lane : wave * 32 + (lane >> 1);
+  const int mine = sched_wave && !PAIR ? lane : (wave & 1) * 32 + (lane >> 1);
   const int32_t base = group * kWave;
   const int32_t i = base + mine;
 
@@ -1069,7 +1150,7 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
   // looks at the request of the same lane in the other rounds wave.
   const ReqPeek own{nf, kb};
   ReqPeek other{0, -1};
-  if (!sched_wave) other = req_peek<MODE>(a, base + (1 - wave) * 32 + (mine & 31));
+  if (!sched_wave || PAIR) other = req_peek<MODE>(a, base + (1 - (wave & 1)) * 32 + (mine & 31));
   int64_t J = own.nf > other.nf ? own.nf : other.nf;
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) {
@@ -1118,9 +1199,12 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
         if (resume)
           load_digest(a.parents + (int64_t)(a.order ? a.order[i] : i) * 32, h);
 #pragma unroll
-        for (int x = 0; x < 8; ++x) (bnd0 ? L.hb : L.ha)[x][lane] = resume ? h[x] : q.sig[x];
+        for (int x = 0; x < 8; ++x) (bnd0 ? L.hb : L.ha)[x][mine] = resume ? h[x] : q.sig[x];
       }
-      lp_prepare(T0, q.sig, !resume && !q.salted_root, bnd0, L, 0, lane);
+      if (PAIR)
+        lp_prepare_pair(T0, q.sig, !resume && !q.salted_root, bnd0, L, 0, mine, odd);
+      else
+        lp_prepare(T0, q.sig, !resume && !q.salted_root, bnd0, L, 0, lane);
     }
   }
   __syncthreads();
@@ -1190,6 +1274,30 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
         *dst = u32x4{bswap(st[0]), bswap(st[1]), bswap(st[2]), bswap(st[3])};
       }
       __syncthreads();
+    } else if (PAIR) {
+      // ---- schedule waves, two lanes per request
+      uint32_t w[16];
+      if (act) {
+        uint32_t m[16];
+#pragma unroll
+        for (int x = 0; x < 8; ++x) {
+          m[x] = L.ha[x][mine];
+          m[8 + x] = L.hb[x][mine];
+        }
+        lp_pair_window(m, w, odd);
+      }
+      lp_pair_groups<0>(w, L.c1b, mine, odd, act);
+      {
+        // block j + 1's tokens, and the load of block j + 2
+        uint32_t Tn[16];
+        const int64_t jn = j + 1 < nfl ? j + 1 : nfl - 1;
+        take_block(nxt, Tn, tp, jn, nfl);
+        if (next) {
+          const bool bnd_next = MODE == KVGOV_BOUNDARY && j + 1 == kb;
+          lp_prepare_pair(Tn, q.sig, false, bnd_next, L, nb, mine, odd);
+        }
+      }
+      __syncthreads();
     } else {
       // ---- schedule wave (an idle wave only meets the barriers)
       uint32_t w[16];
@@ -1219,10 +1327,10 @@ __device__ __forceinline__ void lp_group(const ChainArgs &a, int32_t group, LpLd
   }
 }
 
-template <int MODE>
-__global__ __launch_bounds__(kLpThreads) void k_chains_lp(ChainArgs a) {
+template <int MODE, bool PAIR>
+__global__ __launch_bounds__(4 * kWave) void k_chains_lp(ChainArgs a) {
   __shared__ LpLds L;
-  lp_group<MODE>(a, blockIdx.x, L);
+  lp_group<MODE, PAIR>(a, blockIdx.x, L);
 }
 
 // Large ordered batches: the first `lp_groups` workgroups run the lane-pair
@@ -1234,7 +1342,7 @@ template <int MODE>
 __global__ __launch_bounds__(256) void k_chains_mixed(ChainArgs a, int32_t lp_groups) {
   __shared__ LpLds L;
   if ((int32_t)blockIdx.x < lp_groups)
-    lp_group<MODE>(a, blockIdx.x, L);
+    lp_group<MODE, true>(a, blockIdx.x, L);
   else
     single_chain<MODE>(a, lp_groups * kWave + ((int32_t)blockIdx.x - lp_groups) * 256 +
                               (int32_t)threadIdx.x);
@@ -1492,12 +1600,24 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
     // lane pairs: two rounds waves and a schedule wave per 64 requests, one
     // or two workgroups per CU; every request of the batch is resident from
     // the start, so the order of the requests does not matter
-    const dim3 grid((unsigned)ceil_div(n, kWave)), block(kLpThreads);
+    // (one workgroup per CU: a fourth wave, which shares the schedule;
+    // two: three waves, the schedule on one)
+    const dim3 grid((unsigned)ceil_div(n, kWave));
     const size_t lds = lp_lds_reserve(slots);
-    switch (mode) {
-      case KVGOV_NONE: hipLaunchKernelGGL(k_chains_lp<KVGOV_NONE>, grid, block, lds, s, a); break;
-      case KVGOV_ROOT: hipLaunchKernelGGL(k_chains_lp<KVGOV_ROOT>, grid, block, lds, s, a); break;
-      default: hipLaunchKernelGGL(k_chains_lp<KVGOV_BOUNDARY>, grid, block, lds, s, a); break;
+    if (slots == 1) {
+      const dim3 block(4 * kWave);
+      switch (mode) {
+        case KVGOV_NONE: hipLaunchKernelGGL((k_chains_lp<KVGOV_NONE, true>), grid, block, lds, s, a); break;
+        case KVGOV_ROOT: hipLaunchKernelGGL((k_chains_lp<KVGOV_ROOT, true>), grid, block, lds, s, a); break;
+        default: hipLaunchKernelGGL((k_chains_lp<KVGOV_BOUNDARY, true>), grid, block, lds, s, a); break;
+      }
+    } else {
+      const dim3 block(kLpThreads);
+      switch (mode) {
+        case KVGOV_NONE: hipLaunchKernelGGL((k_chains_lp<KVGOV_NONE, false>), grid, block, lds, s, a); break;
+        case KVGOV_ROOT: hipLaunchKernelGGL((k_chains_lp<KVGOV_ROOT, false>), grid, block, lds, s, a); break;
+        default: hipLaunchKernelGGL((k_chains_lp<KVGOV_BOUNDARY, false>), grid, block, lds, s, a); break;
+      }
     }
   } else {
     // More than two lane-pair workgroups per CU: the batch has at least as
