@@ -202,11 +202,9 @@ struct LookupArgs {
 
 // G lanes per request take G consecutive blocks at a time; a ballot over the
 // group finds the first miss, and the group stops at the first chunk that
-// holds one.  A probe reads its key's bucket (one 128-byte line) at once:
-// loads of single slots, the later ones hitting the line in the cache, and
-// several probes in flight per lane (over blocks past the first miss) both
-// measured slower on the probe-heavy workload, whose lookup is bound by the
-// lines it moves.
+// holds one.  Several probes in flight per lane (over blocks past the first
+// miss: 2 or 4 per lane) measured slower on the probe-heavy workload, whose
+// lookup is bound by the lines it moves rather than by latency.
 template <int G>
 __global__ __launch_bounds__(256) void k_lookup(LookupArgs a) {
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
