@@ -17,10 +17,11 @@ full block, both modes).  The roofline entry is for the chain kernel (the
 dominant kernel), its fraction taken on 1672 integer ops per compression
 (the FIPS 180-4 definition, one op per rotate, shift, xor, and, add or
 3-input add; the gfx950 count with 3-input logic ops, 1384, is beside it).
-The timed steps carry HIP events around the chain launches only (a timing
-event costs its stream a few microseconds); the per-phase launch times come
-from as many steps again, run after the timed ones with events around every
-call.
+The timed steps carry HIP events around the chain kernels only (the
+library records them around the kernel itself, after the ordering kernels
+of a large batch; a timing event costs its stream a few microseconds); the
+per-phase launch times come from as many steps again, run after the timed
+ones with events around every call.
 
 After the line's own workload, the default run times the other
 configurations, each with its own kind of step, and summarises each under
@@ -176,6 +177,10 @@ KERNEL_SOURCES = {
     "radix": ["radix.hip", "table.h", "common.h"],
 }
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "hbm_traffic.md")
+TRAFFIC_FRAC_NOTE = ("HBM bytes the kernel actually moves per launch (traffic) over its mean "
+                     "duration, against the same peak: how busy the memory is, where frac "
+                     "counts algorithmic bytes only (a 32-byte slot probe fills a 128-byte "
+                     "line)")
 
 
 def sources_sha256(group: str) -> str:
@@ -887,14 +892,14 @@ def run_workload(name: str, args, dev, K, torch):
             s.wait_event(salted)
             if not probe_only:
                 if chains_ev:
-                    e0 = torch.cuda.Event(enable_timing=True)
-                    e1 = torch.cuda.Event(enable_timing=True)
-                    e0.record(s)
+                    # the library records this pair around the chain kernel
+                    # itself (not the ordering kernels before it)
+                    e0, e1 = chain_events.pop()
+                    K.time_next_chain_kernel(e0, e1)
                 hash_call(m, s)
                 # the chains' end (the salts buffer they read may be
                 # rewritten after it); the timing event serves when there is one
                 if chains_ev:
-                    e1.record(s)
                     ev_chain.append((m, e0, e1))
                     cd = e1
                 else:
@@ -967,6 +972,14 @@ def run_workload(name: str, args, dev, K, torch):
     log(f"warmup {args.warmup} steps ({depth} batch(es) in flight)")
     for i in range(args.warmup):
         step(i, False, False)
+    torch.cuda.synchronize()
+    # timing events of the chain kernels, created (by a first record) before
+    # the timed region, which then holds only the library's records of them
+    chain_events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                    for _ in range(args.steps * len(modes))]
+    for e0, e1 in chain_events:
+        e0.record()
+        e1.record()
     torch.cuda.synchronize()
     log(f"timing {args.steps} steps")
     t0 = time.perf_counter()
@@ -1112,6 +1125,9 @@ def run_workload(name: str, args, dev, K, torch):
         "bound": "hbm", "kernel": "k_lookup (first-miss prefix lookup)",
         "achieved": look_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
         "frac": look_gbs / HBM_PEAK_GBS, "traffic": None if ltr is None else ltr["bytes"],
+        "traffic_frac": None if ltr is None else
+        ltr["bytes"] / float(np.mean(list(look_mean.values()))) / 1e9 / HBM_PEAK_GBS,
+        "traffic_frac_note": TRAFFIC_FRAC_NOTE,
         "bytes_per_launch": {W.MODE_NAMES[m]: b for m, b in look_bytes.items()},
         "launch_ms": {W.MODE_NAMES[m]: t * 1e3 for m, t in look_mean.items()},
         "examined_blocks_per_launch": {
@@ -1355,10 +1371,14 @@ def run_workload(name: str, args, dev, K, torch):
     if not probe_only and not admission and not radix_cfg:
         ins_gbs = float(np.mean([phases[W.MODE_NAMES[m]]["insert"]["gbs"] for m in modes]))
         itr = recorded_traffic("k_insert<false>", wl.name, "cache")
+        ins_s = float(np.mean([phases[W.MODE_NAMES[m]]["insert"]["ms_median"]
+                               for m in modes])) / 1e3
         result["roofline_insert"] = {
             "bound": "hbm", "kernel": "k_insert (set-union insert)", "achieved": ins_gbs,
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ins_gbs / HBM_PEAK_GBS,
             "traffic": None if itr is None else itr["bytes"],
+            "traffic_frac": None if itr is None else itr["bytes"] / ins_s / 1e9 / HBM_PEAK_GBS,
+            "traffic_frac_note": TRAFFIC_FRAC_NOTE,
             "bytes_note": f"{INSERT_BYTES_NEW} B per new key (query read, slot read, slot "
                           f"write), {INSERT_BYTES_PRESENT} B per present key",
         }
@@ -1539,12 +1559,12 @@ def main():
     result, ok = run_workload(args.config, args, dev, K, torch)
     if args.config == HEADLINE and not args.no_configs:
         # the other configs, each a bench of its own kind after the headline
-        # (fewer steps, no extras, no CPU timing; the oracle's sampled
-        # bit-exact gate still runs unless --no-cpu-baseline)
+        # (at most 30 timed steps, no extras, no CPU timing; the oracle's
+        # sampled bit-exact gate still runs unless --no-cpu-baseline)
         configs = {args.config: summarize(result)}
         for name in SECONDARY:
             sub = argparse.Namespace(**vars(args))
-            sub.steps, sub.warmup = min(args.steps, 10), min(args.warmup, 2)
+            sub.steps, sub.warmup = min(args.steps, 30), min(args.warmup, 5)
             sub.no_extras, sub.cpu_timing, sub.mode = True, False, "all"
             r, ok_r = run_workload(name, sub, dev, K, torch)
             ok &= ok_r

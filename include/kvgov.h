@@ -178,6 +178,23 @@ int kvgov_hash_chains_noalloc(const int32_t *tokens, int64_t n_tokens,
                               int32_t *status, void *stream);
 
 /*
+ * Measurement of the chain kernel alone.  A chain call (kvgov_hash_chains,
+ * _noalloc or _resume) enqueues, for large batches, the longest-first
+ * ordering before its chain kernel; events recorded around the call measure
+ * both.  After this call, the next chain call made by the same host thread
+ * records start_event on its stream immediately before the chain kernel's
+ * launch and end_event immediately after it, so that the elapsed time
+ * between them is the kernel's.  The events are the caller's (hipEvent_t,
+ * created with timing enabled, alive until used); the library keeps only
+ * the two pointers and forgets them when that next chain call starts,
+ * whatever it returns.  A call that returns before launching (an argument
+ * error, n == 0) records neither event.  NULL, NULL clears a pending pair.
+ * Errors: KVGOV_E_INVAL if exactly one pointer is NULL (nothing changes).
+ * The chain call returns KVGOV_E_HIP if recording an event fails.
+ */
+int kvgov_time_next_chain_kernel(void *start_event, void *end_event);
+
+/*
  * Chain extension (Sec. 2.1; Sec. 5.7 on multi-turn sessions, where turn
  * n+1 extends turn n exactly).  Because h_j depends only on h_{j-1}, T_j and,
  * for the salted block, sigma_p, a chain whose digests up to block j0 - 1 are

@@ -1554,12 +1554,18 @@ static const int32_t *order_requests(const int64_t *blk_offsets, int32_t n, int3
   return order;
 }
 
+// Events the next chain call of this host thread records around its chain
+// kernel (kvgov_time_next_chain_kernel); taken and cleared by that call.
+static thread_local hipEvent_t t_chain_events[2] = {nullptr, nullptr};
+
 static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_offsets,
                             int32_t n, const int32_t *principal, const uint8_t *salts, int32_t P,
                             int32_t mode, const int32_t *boundary_tok, int32_t block_size,
                             const int32_t *start, const uint8_t *parents,
                             const int64_t *blk_offsets, uint8_t *hashes, int64_t n_blocks,
                             int32_t *status, void *stream, bool noalloc) {
+  const hipEvent_t ev_start = t_chain_events[0], ev_end = t_chain_events[1];
+  t_chain_events[0] = t_chain_events[1] = nullptr;
   if (n < 0 || n_tokens < 0 || n_blocks < 0 || !status) return KVGOV_E_INVAL;
   if (mode != KVGOV_NONE && mode != KVGOV_ROOT && mode != KVGOV_BOUNDARY) return KVGOV_E_INVAL;
   if (block_size != KVGOV_BLOCK_SIZE) return KVGOV_E_UNSUPPORTED;
@@ -1604,6 +1610,7 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
     // two: three waves, the schedule on one)
     const dim3 grid((unsigned)ceil_div(n, kWave));
     const size_t lds = lp_lds_reserve(slots);
+    if (ev_start && hipEventRecord(ev_start, s) != hipSuccess) return KVGOV_E_HIP;
     if (slots == 1) {
       const dim3 block(4 * kWave);
       switch (mode) {
@@ -1643,6 +1650,10 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
     const dim3 grid((unsigned)(lp_groups + ceil_div(rest, 4 * kWave))), block(4 * kWave);
     const size_t res = chain_lds_reserve();
     const size_t lds = res > sizeof(LpLds) ? res - sizeof(LpLds) : 0;
+    if (ev_start && hipEventRecord(ev_start, s) != hipSuccess) {
+      if (owned) (void)hipFreeAsync(owned, s);
+      return KVGOV_E_HIP;
+    }
     switch (mode) {
       case KVGOV_NONE: hipLaunchKernelGGL(k_chains_mixed<KVGOV_NONE>, grid, block, lds, s, a, lp_groups); break;
       case KVGOV_ROOT: hipLaunchKernelGGL(k_chains_mixed<KVGOV_ROOT>, grid, block, lds, s, a, lp_groups); break;
@@ -1650,8 +1661,16 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
     }
   }
   int rc = launch_status();
+  if (ev_end && hipEventRecord(ev_end, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
   if (owned && hipFreeAsync(owned, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
   return rc;
+}
+
+int kvgov_time_next_chain_kernel(void *start_event, void *end_event) {
+  if ((start_event == nullptr) != (end_event == nullptr)) return KVGOV_E_INVAL;
+  t_chain_events[0] = static_cast<hipEvent_t>(start_event);
+  t_chain_events[1] = static_cast<hipEvent_t>(end_event);
+  return KVGOV_OK;
 }
 
 int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens, const int64_t *tok_offsets,

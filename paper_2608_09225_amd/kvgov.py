@@ -12,6 +12,7 @@ Calls mirror the C ABI one to one:
     kvgov_block_offsets -> block_offsets(tok_offsets)
     kvgov_hash_chains   -> hash_chains(tokens, tok_offsets, principal, salts, mode, ...)
     kvgov_hash_chains_noalloc -> hash_chains_noalloc(..., blk_offsets, out, status)
+    kvgov_time_next_chain_kernel -> time_next_chain_kernel(start_event, end_event)
     kvgov_hash_chains_resume -> hash_chains_resume(..., start_block, parents, ...)
     kvgov_resume_offsets -> resume_offsets(tok_offsets, start_block)
     kvgov_cache_*       -> Cache(log2_slots).insert / lookup / admit / set_recency / evict /
@@ -47,6 +48,7 @@ _SIGNATURES = {
     "kvgov_hash_chains_noalloc": (ctypes.c_int, [_vp, _c_i64, _vp, _c_i32, _vp, _vp, _c_i32,
                                                  _c_i32, _vp, _c_i32, _vp, _vp, _c_i64, _vp,
                                                  _vp]),
+    "kvgov_time_next_chain_kernel": (ctypes.c_int, [_vp, _vp]),
     "kvgov_hash_chains_resume": (ctypes.c_int, [_vp, _c_i64, _vp, _c_i32, _vp, _vp, _c_i32,
                                                 _c_i32, _vp, _c_i32, _vp, _vp, _vp, _vp,
                                                 _c_i64, _vp, _vp]),
@@ -277,6 +279,24 @@ def resume_offsets(tok_offsets: torch.Tensor, start_block: torch.Tensor,
     if own:
         check_status(status, "kvgov_resume_offsets")
     return out
+
+
+def time_next_chain_kernel(start: Optional[torch.cuda.Event],
+                           end: Optional[torch.cuda.Event]) -> None:
+    """kvgov_time_next_chain_kernel: the next chain call of this thread records
+    `start` and `end` (timing events) around its chain kernel alone.  The
+    events must exist on the device already (torch creates an event at its
+    first record), so each is recorded once here if it has not been."""
+    if start is None and end is None:
+        _check(lib().kvgov_time_next_chain_kernel(None, None), "kvgov_time_next_chain_kernel")
+        return
+    for e in (start, end):
+        if e is None:
+            raise ValueError("time_next_chain_kernel: both events or neither")
+        if not e.cuda_event:
+            e.record()
+    _check(lib().kvgov_time_next_chain_kernel(_vp(start.cuda_event), _vp(end.cuda_event)),
+           "kvgov_time_next_chain_kernel")
 
 
 def hash_chains_resume(tokens: torch.Tensor, tok_offsets: torch.Tensor,

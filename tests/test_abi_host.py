@@ -183,3 +183,19 @@ def test_peaks_library_exports_and_validates():
     assert L.kvgov_peak_gather(fake, 0, fake, 4, 4, ctypes.byref(n), None) == inval
     assert L.kvgov_peak_gather(ctypes.c_void_p(0x1008), 16, fake, 4, 4, ctypes.byref(n),
                                None) == inval
+
+
+def test_chain_kernel_timing_hook_host_rules():
+    c = K.header_constants()
+    L = K.lib()
+    fake = ctypes.c_void_p(0x1000)  # never recorded: the chain call below fails first
+    assert L.kvgov_time_next_chain_kernel(None, None) == 0
+    assert L.kvgov_time_next_chain_kernel(fake, None) == c["KVGOV_E_INVAL"]
+    assert L.kvgov_time_next_chain_kernel(None, fake) == c["KVGOV_E_INVAL"]
+    try:
+        assert L.kvgov_time_next_chain_kernel(fake, fake) == 0
+        # a chain call takes the pending pair, whatever it returns
+        assert L.kvgov_hash_chains(None, 0, None, -1, None, None, 0, 0, None, 16, None, None,
+                                   0, fake, None) == c["KVGOV_E_INVAL"]
+    finally:
+        assert L.kvgov_time_next_chain_kernel(None, None) == 0
