@@ -35,10 +35,13 @@
  *   - K and the salts are secrets: the library keeps no copy of K after
  *     kvgov_salts returns and logs nothing.
  *   - The calls allocate no device memory except kvgov_cache_create,
- *     kvgov_radix_create and the stream-ordered scratch of
- *     kvgov_hash_chains and its resume variant, of kvgov_cache_admit, of
- *     the maintenance calls (see there) and of the offset helpers (8 bytes
- *     per 1024 requests).
+ *     kvgov_radix_create, the stream-ordered scratch of the maintenance
+ *     calls (see there), and the per-stream scratch that kvgov_hash_chains
+ *     and its resume variant, kvgov_cache_admit and the offset helpers use:
+ *     one buffer per (device, stream) the library has seen, grown on demand
+ *     (growth waits for that stream, then frees the old buffer) and held
+ *     until the process ends.  A stream runs its work in order, so its
+ *     buffer serves one call at a time and no memory passes between streams.
  */
 #ifndef KVGOV_H
 #define KVGOV_H
@@ -76,7 +79,7 @@ extern "C" {
 #define KVGOV_E_NOMEM (-8)       /* device allocation failed */
 #define KVGOV_E_CAPACITY (-9)    /* export buffer smaller than the key count */
 #define KVGOV_E_DEVICE (-10)     /* cache used with another device current */
-#define KVGOV_E_INTERNAL (-11)   /* kernel: a bounded wait ran out (never expected) */
+#define KVGOV_E_INTERNAL (-11)   /* kernel: an internal invariant failed (never expected) */
 #define KVGOV_E_TOO_LARGE (-12)  /* batch above the allocation-free entry point's limit */
 
 /* Largest batch (requests) of kvgov_hash_chains_noalloc. */
@@ -142,9 +145,12 @@ int kvgov_block_offsets(const int64_t *tok_offsets, int32_t n, int32_t block_siz
  *              error (KVGOV_E_OFFSETS / _PRINCIPAL / _BOUNDARY) there and skip
  *              the offending request.
  * Scratch: batches of more than two 64-request lane-pair workgroups per CU
- * (n > 128 * CUs) are ordered longest first using 4 * (4096 + n) bytes from
- * hipMallocAsync on `stream`, freed in stream order.
- * Errors: KVGOV_E_INVAL, KVGOV_E_UNSUPPORTED, KVGOV_E_NOMEM, KVGOV_E_HIP.
+ * (n > 128 * CUs) are ordered longest first using 4 * (4096 + n) bytes of
+ * the stream's scratch (see the notes at the top).
+ * Errors: KVGOV_E_INVAL, KVGOV_E_UNSUPPORTED, KVGOV_E_NOMEM, KVGOV_E_HIP;
+ * KVGOV_E_INTERNAL latched in `status` if the ordering scratch held an
+ * index outside the batch (never expected: it would mean the scratch was
+ * overwritten during the call).
  */
 int kvgov_hash_chains(const int32_t *tokens, int64_t n_tokens,
                       const int64_t *tok_offsets, int32_t n,
@@ -302,8 +308,8 @@ int kvgov_cache_lookup(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk
  * hashes, blk_offsets, n, n_blocks as for kvgov_cache_insert.
  * hit_blocks, new_blocks  device out, int32 [n].
  * n_new        host out or NULL, as for kvgov_cache_insert.
- * Scratch: 4 * n_blocks bytes from hipMallocAsync on `stream`, freed in
- * stream order.
+ * Scratch: 4 * n_blocks bytes of the stream's scratch (see the notes at
+ * the top).
  * Kernel errors: KVGOV_E_OFFSETS (latched; outputs of the batch are not
  * meaningful, rows of requests found malformed are set to 0), KVGOV_E_FULL
  * (latched; keys that found no slot count as not visible and not new).

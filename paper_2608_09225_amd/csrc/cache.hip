@@ -962,15 +962,16 @@ int kvgov_cache_admit(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_
     return KVGOV_OK;
   }
   hipStream_t s = as_stream(stream);
-  uint32_t *codes = nullptr;
-  if (hipMallocAsync(reinterpret_cast<void **>(&codes),
-                     sizeof(uint32_t) * (size_t)std::max<int64_t>(n_blocks, 1), s) != hipSuccess)
-    return KVGOV_E_NOMEM;
+  // per-row codes of the insert, in the stream's scratch (held while the two
+  // kernels are enqueued)
+  std::unique_lock<std::mutex> lk;
+  void *scratch_p = nullptr;
+  rc = stream_scratch(s, sizeof(uint32_t) * (size_t)std::max<int64_t>(n_blocks, 1), &scratch_p,
+                      lk);
+  if (rc != KVGOV_OK) return rc;
+  uint32_t *codes = static_cast<uint32_t *>(scratch_p);
   const uint32_t epoch = c->epoch.fetch_add(1) + 1;
-  if (epoch == 0xFFFFFFFFu) {
-    (void)hipFreeAsync(codes, s);
-    return KVGOV_E_UNSUPPORTED;
-  }
+  if (epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;
   hipLaunchKernelGGL(k_insert<true>, dim3(insert_grid(n_blocks)), dim3(256), 0, s, c->view,
                      hashes, blk_offsets, n, n_blocks, epoch, codes);
   AdmitArgs a{c->view, blk_offsets, n, n_blocks, epoch, codes, hit_blocks, new_blocks};
@@ -984,7 +985,7 @@ int kvgov_cache_admit(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_
     default: hipLaunchKernelGGL(k_admit_scan<64>, grid, block, 0, s, a); break;
   }
   rc = launch_status();
-  if (hipFreeAsync(codes, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
+  lk.unlock();
   if (rc != KVGOV_OK || !n_new) return rc;
   return read_new_keys(c, epoch, n_new, s);
 }

@@ -35,7 +35,10 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <map>
 #include <mutex>
+#include <thread>
+#include <tuple>
 #include <vector>
 
 #include "common.h"
@@ -349,7 +352,8 @@ __global__ __launch_bounds__(256) void k_order_scan(int32_t *hist) {
 
 __global__ __launch_bounds__(kOrderThreads) void k_order_scatter(const int64_t *blk_offsets,
                                                                  int32_t n, int32_t *cursor,
-                                                                 int32_t *order) {
+                                                                 int32_t *order,
+                                                                 int32_t *status) {
   __shared__ int32_t cnt[kOrderBuckets];
   __shared__ int32_t at[kOrderBuckets];
   for (int i = threadIdx.x; i < kOrderBuckets; i += kOrderThreads) cnt[i] = 0;
@@ -373,7 +377,12 @@ __global__ __launch_bounds__(kOrderThreads) void k_order_scatter(const int64_t *
   for (int k = 0; k < kOrderPerThread; ++k) {
     if (bucket[k] >= 0) {
       const int64_t r = base + (int64_t)k * kOrderThreads + threadIdx.x;
-      order[at[bucket[k]] + rank[k]] = (int32_t)r;
+      // the positions are 0 .. n-1 while the histogram is the batch's own
+      const int32_t pos = at[bucket[k]] + rank[k];
+      if ((uint32_t)pos < (uint32_t)n)
+        order[pos] = (int32_t)r;
+      else
+        latch(status, KVGOV_E_INTERNAL);
     }
   }
 }
@@ -423,6 +432,12 @@ struct ChainReq {
 
 template <int MODE>
 __device__ __forceinline__ bool chain_setup(const ChainArgs &a, int32_t r, ChainReq &q) {
+  // r comes from the ordering scratch when the batch is ordered: a value
+  // outside the batch would mean that scratch was overwritten
+  if ((uint32_t)r >= (uint32_t)a.n) {
+    latch(a.status, KVGOV_E_INTERNAL);
+    return false;
+  }
   const int64_t t0 = a.tok_offsets[r], t1 = a.tok_offsets[r + 1];
   if (t0 < 0 || t1 < t0 || t1 > a.n_tokens) {
     latch(a.status, KVGOV_E_OFFSETS);
@@ -1422,6 +1437,42 @@ int device_cu_count() {
   return cus[dev];
 }
 
+int stream_scratch(hipStream_t s, size_t bytes, void **ptr, std::unique_lock<std::mutex> &lk) {
+  static std::mutex mu;
+  // keyed by device and stream; hipStreamPerThread names a different stream
+  // in every host thread, so the thread is part of its key
+  using Key = std::tuple<int, hipStream_t, std::thread::id>;
+  static std::map<Key, std::pair<void *, size_t>> bufs;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return KVGOV_E_HIP;
+  const std::thread::id tid =
+      s == hipStreamPerThread ? std::this_thread::get_id() : std::thread::id();
+  lk = std::unique_lock<std::mutex>(mu);
+  std::pair<void *, size_t> &b = bufs[Key(dev, s, tid)];
+  if (b.second < bytes) {
+    constexpr size_t kGrain = 64 * 1024;
+    const size_t cap = (std::max(bytes, 2 * b.second) + kGrain - 1) / kGrain * kGrain;
+    if (b.first) {
+      // earlier calls on s may still read the old buffer
+      const bool ok = hipStreamSynchronize(s) == hipSuccess && hipFree(b.first) == hipSuccess;
+      b = {nullptr, 0};
+      if (!ok) {
+        lk.unlock();
+        return KVGOV_E_HIP;
+      }
+    }
+    void *p = nullptr;
+    if (hipMalloc(&p, cap) != hipSuccess) {
+      (void)hipGetLastError();  // not left for the next launch check
+      lk.unlock();
+      return KVGOV_E_NOMEM;
+    }
+    b = {p, cap};
+  }
+  *ptr = b.first;
+  return KVGOV_OK;
+}
+
 // Scratch of the allocation-free hashing entry point: the longest-first
 // order of a batch (histogram, then the order), kOrderBuckets + n int32 for
 // n up to KVGOV_NOALLOC_MAX_REQUESTS.  One copy per device, held until the
@@ -1473,7 +1524,8 @@ const char *kvgov_strerror(int code) {
     case KVGOV_E_NOMEM: return "device allocation failed";
     case KVGOV_E_CAPACITY: return "export buffer too small";
     case KVGOV_E_DEVICE: return "cache used with a different current device";
-    case KVGOV_E_INTERNAL: return "bounded wait exhausted inside a kernel";
+    case KVGOV_E_INTERNAL:
+      return "internal invariant failed inside a kernel (bounded wait or scratch contents)";
     case KVGOV_E_TOO_LARGE:
       return "batch above KVGOV_NOALLOC_MAX_REQUESTS requests (allocation-free entry point)";
     default: return "unknown error code";
@@ -1511,18 +1563,17 @@ static int block_offsets_impl(const int64_t *tok_offsets, const int32_t *start, 
   if (block_size != KVGOV_BLOCK_SIZE) return KVGOV_E_UNSUPPORTED;
   hipStream_t s = as_stream(stream);
   const int64_t tiles = std::max<int64_t>(1, ceil_div(n, kScanTile));
-  int64_t *partial = nullptr;
-  if (hipMallocAsync(reinterpret_cast<void **>(&partial), tiles * sizeof(int64_t), s) !=
-      hipSuccess)
-    return KVGOV_E_NOMEM;
+  std::unique_lock<std::mutex> lk;
+  void *scratch_p = nullptr;
+  const int src = stream_scratch(s, (size_t)tiles * sizeof(int64_t), &scratch_p, lk);
+  if (src != KVGOV_OK) return src;
+  int64_t *partial = static_cast<int64_t *>(scratch_p);
   hipLaunchKernelGGL(k_blk_partial, dim3((unsigned)tiles), dim3(kScanThreads), 0, s,
                      tok_offsets, start, n, partial, status);
   hipLaunchKernelGGL(k_blk_scan_partials, dim3(1), dim3(kScanThreads), 0, s, partial, tiles);
   hipLaunchKernelGGL(k_blk_write, dim3((unsigned)tiles), dim3(kScanThreads), 0, s, tok_offsets,
                      start, n, partial, blk_offsets, status);
-  int rc = launch_status();
-  if (hipFreeAsync(partial, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
-  return rc;
+  return launch_status();
 }
 
 int kvgov_block_offsets(const int64_t *tok_offsets, int32_t n, int32_t block_size,
@@ -1541,7 +1592,7 @@ int kvgov_resume_offsets(const int64_t *tok_offsets, const int32_t *start_block,
 // counts) in `buf`: kOrderBuckets + n int32 (the histogram, then the
 // order).  Returns the order.
 static const int32_t *order_requests(const int64_t *blk_offsets, int32_t n, int32_t *buf,
-                                     hipStream_t s) {
+                                     int32_t *status, hipStream_t s) {
   int32_t *hist = buf;
   int32_t *order = buf + kOrderBuckets;
   hipLaunchKernelGGL(k_fill_i32, dim3(kOrderBuckets / 256), dim3(256), 0, s, hist,
@@ -1550,7 +1601,7 @@ static const int32_t *order_requests(const int64_t *blk_offsets, int32_t n, int3
   hipLaunchKernelGGL(k_order_hist, tiles, dim3(kOrderThreads), 0, s, blk_offsets, n, hist);
   hipLaunchKernelGGL(k_order_scan, dim3(1), dim3(256), 0, s, hist);
   hipLaunchKernelGGL(k_order_scatter, tiles, dim3(kOrderThreads), 0, s, blk_offsets, n, hist,
-                     order);
+                     order, status);
   return order;
 }
 
@@ -1601,7 +1652,7 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
   // then takes nearly every issue slot, so the workgroups reserve LDS (unused
   // beyond the kernel's own) to bound how many share a CU.
   const int slots = lp_slots(n);
-  int32_t *owned = nullptr;  // stream-ordered scratch of this call
+  std::unique_lock<std::mutex> lk;  // held while the ordered launch is enqueued
   if (slots) {
     // lane pairs: two rounds waves and a schedule wave per 64 requests, one
     // or two workgroups per CU; every request of the batch is resident from
@@ -1633,27 +1684,25 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
     // requests then run on lane-pair workgroups (one eighth of the CUs), the
     // rest one lane per request; one workgroup per CU.
     // The ordering scratch: the library's fixed array for the
-    // allocation-free entry point, else stream-ordered.
+    // allocation-free entry point, else the stream's own scratch.
     int32_t *buf = nullptr;
     if (noalloc) {
       buf = noalloc_scratch();
       if (!buf) return KVGOV_E_HIP;
     } else {
       const size_t bytes = sizeof(int32_t) * ((size_t)kOrderBuckets + (size_t)n);
-      if (hipMallocAsync(reinterpret_cast<void **>(&owned), bytes, s) != hipSuccess)
-        return KVGOV_E_NOMEM;
-      buf = owned;
+      void *p = nullptr;
+      const int src = stream_scratch(s, bytes, &p, lk);
+      if (src != KVGOV_OK) return src;
+      buf = static_cast<int32_t *>(p);
     }
-    a.order = order_requests(blk_offsets, n, buf, s);
+    a.order = order_requests(blk_offsets, n, buf, status, s);
     const int32_t lp_groups = std::max(1, device_cu_count() / 8);
     const int64_t rest = std::max<int64_t>(0, (int64_t)n - (int64_t)lp_groups * kWave);
     const dim3 grid((unsigned)(lp_groups + ceil_div(rest, 4 * kWave))), block(4 * kWave);
     const size_t res = chain_lds_reserve();
     const size_t lds = res > sizeof(LpLds) ? res - sizeof(LpLds) : 0;
-    if (ev_start && hipEventRecord(ev_start, s) != hipSuccess) {
-      if (owned) (void)hipFreeAsync(owned, s);
-      return KVGOV_E_HIP;
-    }
+    if (ev_start && hipEventRecord(ev_start, s) != hipSuccess) return KVGOV_E_HIP;
     switch (mode) {
       case KVGOV_NONE: hipLaunchKernelGGL(k_chains_mixed<KVGOV_NONE>, grid, block, lds, s, a, lp_groups); break;
       case KVGOV_ROOT: hipLaunchKernelGGL(k_chains_mixed<KVGOV_ROOT>, grid, block, lds, s, a, lp_groups); break;
@@ -1662,7 +1711,6 @@ static int hash_chains_impl(const int32_t *tokens, int64_t n_tokens, const int64
   }
   int rc = launch_status();
   if (ev_end && hipEventRecord(ev_end, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
-  if (owned && hipFreeAsync(owned, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
   return rc;
 }
 

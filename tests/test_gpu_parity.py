@@ -454,3 +454,41 @@ def test_chains_between_one_and_two_pairs_per_cu(n_req):
         want = O.hash_chains_parallel(b.tokens, b.tok_offsets, b.principal, osalts, mode,
                                       b.boundary_tok)
         assert np.array_equal(got, want), mode
+
+
+def test_chains_concurrent_streams_and_scratch_growth():
+    """Ordered batches (above 128 requests per CU) hashed on three streams at
+    once, twice, the second time with larger batches (each stream's scratch
+    grows between the rounds): every digest equals the oracle's and no
+    kernel latches an error."""
+    Kb, ids = secret(21, 29)
+    sd = K.salts(Kb, dev(ids))
+    osalts = O.salts(Kb, ids)
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    main = torch.cuda.current_stream()
+    for rnd, base in enumerate((34000, 52000)):
+        jobs = []
+        for k, s in enumerate(streams):
+            n = base + 3001 * k
+            g = np.random.default_rng(700 + 10 * rnd + k)
+            b = ragged(800 + 10 * rnd + k, g.integers(0, 120, n), P=29)
+            mode = (W.NONE, W.ROOT, W.BOUNDARY)[(k + rnd) % 3]
+            args = [dev(b.tokens), dev(b.tok_offsets), dev(b.principal), dev(b.boundary_tok)]
+            bo = K.block_offsets(args[1])
+            jobs.append((b, mode, args, bo))
+        torch.cuda.synchronize()
+        outs = []
+        for (b, mode, args, bo), s in zip(jobs, streams):
+            s.wait_stream(main)
+            with torch.cuda.stream(s):
+                st = K.new_status()
+                out = torch.empty((int(bo[-1].item()), 32), dtype=torch.uint8, device="cuda")
+                K.hash_chains(args[0], args[1], args[2], sd, mode, args[3], blk_offsets=bo,
+                              out=out, status=st, check=False, stream=s)
+            outs.append((out, st))
+        torch.cuda.synchronize()
+        for (b, mode, _, _), (out, st) in zip(jobs, outs):
+            assert int(st.item()) == 0, (rnd, mode)
+            want = O.hash_chains_parallel(b.tokens, b.tok_offsets, b.principal, osalts, mode,
+                                          b.boundary_tok)
+            assert np.array_equal(out.cpu().numpy(), want), (rnd, mode)
