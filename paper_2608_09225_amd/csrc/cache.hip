@@ -8,8 +8,8 @@
 // Layout (HBM):
 //   keys [slots][32 B]  the stored keys; an empty slot holds 32 bytes 0xFF.
 //                       Lookups read only this array: a probe is one 32-byte
-//                       read, and four consecutive slots share a 128-byte line,
-//                       so linear probing mostly stays in one line.
+//                       read, and a probe sequence runs through the four
+//                       slots of its 128-byte line before it leaves it.
 //   tags [slots] u64    0 = empty, else (epoch << 32) | (claimant + 1): the
 //                       insert call that claimed the slot and the index of the
 //                       claiming key within that call's input.
@@ -78,7 +78,7 @@ __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long l
   }
 }
 
-// Consecutive keys per wave chunk of the insert.  Longer chunks mean fewer
+// Consecutive keys per wave chunk of the admission insert.  Longer chunks mean fewer
 // waves in flight at once, so that the copies of a key that many requests
 // hold (a principal's shared prefix) reach its slot over a longer span and
 // most of them find it claimed by a plain read instead of racing for it
@@ -86,7 +86,7 @@ __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long l
 constexpr int kInsChunk = 256;
 
 // The largest r in [0, n) with bo[r] <= f (bo non-decreasing in a valid
-// batch; any answer in range is harmless otherwise, see k_insert).  Every
+// batch; any answer in range is harmless otherwise, see k_admit_insert).  Every
 // lane of a wave searches the same f.
 __device__ __forceinline__ int32_t find_request(const int64_t *bo, int32_t n, int64_t f) {
   int32_t a = 0, b = n - 1;
@@ -97,32 +97,29 @@ __device__ __forceinline__ int32_t find_request(const int64_t *bo, int32_t n, in
   return a;
 }
 
-// Batched insert.  A wave takes chunks of kInsChunk consecutive keys, 64 at
-// a time.  Before touching the table a key is compared with the key at the
-// same block position of the previous request (requests that share a prefix
-// - the same principal, or any principal below the boundary block - hold
-// the same keys there): an equal earlier key makes this one a duplicate
-// that needs no table access, so a prefix shared by thousands of requests
-// costs a few table operations per key instead of thousands of atomics on
-// one slot.  The request of each key comes from a window of 64 request
-// starts (a search over lanes); the comparison is only an optimisation:
-// skipping a key that equals an earlier key of the batch is always correct
-// (the earlier one is inserted, or is itself a duplicate of an earlier
-// one), and the compared position is checked to lie in the batch, so
-// malformed interior offsets cannot cause a wrong result or an
-// out-of-range read.  A row's request, and so its depth (its position in
-// the request, which the recency rank holds), is exact: rows whose request
-// lies past the window search for it.
-//
-// ADMIT: also the admission's first half: claims are lowered to the
-// earliest row, and codes[f] records where row f's key went (kCodeDup for a
-// key skipped as equal to the previous request's, which is in an earlier
-// request by construction).
-template <bool ADMIT>
-__global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hashes,
-                                                const int64_t *blk_offsets, int32_t n,
-                                                int64_t n_blocks, uint32_t epoch,
-                                                uint32_t *codes) {
+// First half of the admission: the insert of the batch's rows, with claims
+// lowered to the earliest row, and codes[f] recording where row f's key went
+// (kCodeDup for a key skipped as equal to the previous request's, which is
+// in an earlier request by construction).  A wave takes chunks of kInsChunk
+// consecutive rows, 64 at a time.  Before touching the table a key is
+// compared with the key at the same block position of the previous request
+// (requests that share a prefix - the same principal, or any principal
+// below the boundary block - hold the same keys there): an equal earlier
+// key makes this one a duplicate that needs no table access, so a prefix
+// shared by thousands of requests costs a few table operations per key
+// instead of thousands of atomics on one slot.  The request of each key
+// comes from a window of 64 request starts (a search over lanes); the
+// comparison is only an optimisation: skipping a key that equals an
+// earlier key of the batch is always correct (the earlier one is inserted,
+// or is itself a duplicate of an earlier one), and the compared position
+// is checked to lie in the batch, so malformed interior offsets cannot
+// cause a wrong result or an out-of-range read.  A row's request, and so
+// its depth (its position in the request, which the recency rank holds),
+// is exact: rows whose request lies past the window search for it.
+__global__ __launch_bounds__(256) void k_admit_insert(TableView t, const uint8_t *hashes,
+                                                      const int64_t *blk_offsets, int32_t n,
+                                                      int64_t n_blocks, uint32_t epoch,
+                                                      uint32_t *codes) {
   __shared__ uint32_t lds4[4];
   const int64_t lo = blk_offsets[0], hi = blk_offsets[n];
   const bool first = blockIdx.x == 0 && threadIdx.x == 0;
@@ -177,10 +174,98 @@ __global__ __launch_bounds__(256) void k_insert(TableView t, const uint8_t *hash
         // the depth of the key: its row within its request (clamped; only
         // malformed interior offsets put it outside [0, 2^31))
         const uint32_t depth = (uint32_t)(jj < 0 ? 0 : (jj > 0x7FFFFFFF ? 0x7FFFFFFF : jj));
-        if (!dup) added += insert_key<ADMIT>(t, key, f, lo, hashes, epoch, &code, depth);
-        if (ADMIT) codes[f] = code;
+        if (!dup) added += insert_key<true>(t, key, f, lo, hashes, epoch, &code, depth);
+        codes[f] = code;
       }
       rc = __shfl(r, 63, 64);
+    }
+  }
+  const uint32_t total = block_sum(added, lds4);
+  if (threadIdx.x == 0 && total) {
+    const int cl = blockIdx.x % kCounterLanes;
+    atomicAdd(&t.meta->new_keys[epoch & 1][cl], (unsigned long long)total);
+    atomicAdd(&t.meta->n_keys[cl], (unsigned long long)total);
+  }
+}
+
+// Plain (set-union) insert with G lanes per request, which walk the
+// request's rows G at a time.  Two comparisons keep keys that many requests
+// share away from the table (a key skipped by either equals a row of the
+// batch that lies before it, and the earliest row of any key is never
+// skipped, so every key reaches the table):
+//   * the previous request's row at the same depth (requests that share a
+//     prefix and are adjacent, e.g. a prefix below the boundary block that
+//     every request holds);
+//   * the row at the same depth of an earlier request that starts with the
+//     same key: the group's first lane inserts the request's first row
+//     before the others start, and if the slot's tag names an earlier row
+//     (the request that claimed the key, mostly the earliest one, since
+//     workgroups start in request order) the group compares against the
+//     rows that follow it.  Requests of one principal share the
+//     root-salted prefix but are rarely adjacent.  (Lowering the tag to the
+//     earliest first row with an atomic minimum, as admission does, measured
+//     slower: 35.7 -> 36.6 us for the paper-shaped root-mode insert.)
+// On a table that tracks recency only the first comparison is made (the
+// second one's row may lie past the end of that request, at another depth,
+// and a key's rank holds its smallest depth).
+// Each request inserts the rows [blk_offsets[r], blk_offsets[r + 1]) cut to
+// the batch [blk_offsets[0], blk_offsets[n]); requests whose offsets are out
+// of order insert nothing.  With non-decreasing offsets that is every row
+// once.  Otherwise every row of the batch still lies in some request's
+// range (take the last r with blk_offsets[r] <= row), so the table receives
+// exactly the batch's keys.
+template <int G>
+__global__ __launch_bounds__(256) void k_insert_req(TableView t, const uint8_t *hashes,
+                                                    const int64_t *blk_offsets, int32_t n,
+                                                    int64_t n_blocks, uint32_t epoch) {
+  __shared__ uint32_t lds4[4];
+  const int64_t lo = blk_offsets[0], hi = blk_offsets[n];
+  if (blockIdx.x == 0 && threadIdx.x < kCounterLanes)
+    t.meta->new_keys[(epoch + 1) & 1][threadIdx.x] = 0;  // counters of the next call
+  if (lo < 0 || hi < lo || hi > n_blocks || hi - lo >= 0xFFFFFFFFll) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicCAS(&t.meta->status, 0, KVGOV_E_OFFSETS);
+    return;
+  }
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t r = gid / G;
+  const int sub = (int)(gid % G);
+  const int lane = threadIdx.x & 63;
+  const int base = lane & ~(G - 1);
+  uint32_t added = 0;
+  // groups never straddle r < n (256 % G == 0); the block sum below needs
+  // every thread, so out-of-range groups only skip the work
+  if (r < n) {
+    const int64_t b_r = blk_offsets[r], b_e = blk_offsets[r + 1];
+    const int64_t b_p = r >= 1 ? blk_offsets[r - 1] : 0;
+    const int64_t b0 = b_r > lo ? b_r : lo, b1 = b_e < hi ? b_e : hi;
+    // the previous request's rows, when its range is in order and in the batch
+    const int64_t n_p = r >= 1 && b_p >= lo && b_p <= b_r ? b_r - b_p : 0;
+    if (b0 < b1) {
+      // first row, by the group's first lane
+      int64_t g0 = -1;
+      if (sub == 0) {
+        const int64_t jj = b0 - b_r;
+        const Key key = load_key(hashes + b0 * 32);
+        const bool dup = jj < n_p && key_eq(key, load_key(hashes + (b_p + jj) * 32));
+        if (!dup) {
+          uint32_t code;
+          unsigned long long claim = 0;
+          added += insert_key<false>(t, key, b0, lo, hashes, epoch, &code, (uint32_t)jj, &claim);
+          const int64_t c = lo + (int64_t)(claim & 0xFFFFFFFFull) - 1;
+          if (!t.track && jj == 0 && (uint32_t)(claim >> 32) == epoch && c >= lo && c < b0)
+            g0 = c;
+        }
+      }
+      g0 = __shfl(g0, base, 64);
+      for (int64_t f = b0 + 1 + sub; f < b1; f += G) {
+        const int64_t jj = f - b_r;
+        const Key key = load_key(hashes + f * 32);
+        bool dup = jj < n_p && key_eq(key, load_key(hashes + (b_p + jj) * 32));
+        if (!dup && g0 >= 0) dup = key_eq(key, load_key(hashes + (g0 + jj) * 32));
+        uint32_t code;
+        const uint32_t depth = (uint32_t)(jj > 0x7FFFFFFF ? 0x7FFFFFFF : jj);
+        if (!dup) added += insert_key<false>(t, key, f, lo, hashes, epoch, &code, depth);
+      }
     }
   }
   const uint32_t total = block_sum(added, lds4);
@@ -244,7 +329,7 @@ struct AdmitArgs {
   int32_t n;
   int64_t n_blocks;
   uint32_t epoch;
-  const uint32_t *codes;  // per row, from k_insert<true>
+  const uint32_t *codes;  // per row, from k_admit_insert
   int32_t *hit_blocks;
   int32_t *new_blocks;
 };
@@ -256,7 +341,7 @@ struct AdmitArgs {
 //                      before b0 (an earlier request holds it);
 //   new for r     <=>  K's earliest row is f itself.
 // hit_blocks[r] = first row not visible (relative to b0), new_blocks[r] =
-// rows new for r.  The earliest rows are final: k_insert<true> has ended.
+// rows new for r.  The earliest rows are final: k_admit_insert has ended.
 template <int G>
 __global__ __launch_bounds__(256) void k_admit_scan(AdmitArgs a) {
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -268,7 +353,7 @@ __global__ __launch_bounds__(256) void k_admit_scan(AdmitArgs a) {
   const uint64_t gmask = group_mask<G>(base);
   const int64_t lo = a.blk_offsets[0], hi = a.blk_offsets[a.n];
   const int64_t b0 = a.blk_offsets[r], b1 = a.blk_offsets[r + 1];
-  // the batch check of k_insert (which then wrote no codes), and this
+  // the batch check of k_admit_insert (which then wrote no codes), and this
   // request's rows inside the batch
   if (lo < 0 || hi < lo || hi > a.n_blocks || hi - lo >= 0xFFFFFFFFll || b0 < lo || b1 < b0 ||
       b1 > hi) {
@@ -733,7 +818,16 @@ int enqueue_clear(kvgov_cache *c, hipStream_t s) {
   return launch_status();
 }
 
-// Waves of 4 x kInsChunk keys, at most 16 workgroups per CU.
+// Lanes per request of the plain insert: about one lane per two rows of
+// the average request, 4 to 64.
+int insert_group(int32_t n, int64_t n_blocks) {
+  const int64_t avg = n > 0 ? n_blocks / n : 0;
+  int g = 4;
+  while (g < 64 && (int64_t)g * 2 < avg) g <<= 1;
+  return g;
+}
+
+// Admission insert: waves of 4 x kInsChunk keys, at most 16 workgroups per CU.
 unsigned insert_grid(int64_t n_blocks) {
   const int64_t groups = ceil_div(std::max<int64_t>(n_blocks, 1), (int64_t)kInsChunk * 4);
   return (unsigned)std::min<int64_t>(groups, (int64_t)device_cu_count() * 16);
@@ -828,8 +922,21 @@ int kvgov::cache_insert_rows(kvgov_cache *c, const uint8_t *hashes, const int64_
                              int32_t n, int64_t n_blocks, hipStream_t s, uint32_t *epoch) {
   *epoch = c->epoch.fetch_add(1) + 1;
   if (*epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;  // 2^32 - 1 inserts since clear
-  hipLaunchKernelGGL(k_insert<false>, dim3(insert_grid(n_blocks)), dim3(256), 0, s, c->view,
-                     hashes, blk_offsets, n, n_blocks, *epoch, nullptr);
+  if (n == 0) {
+    // no request: only the batch check and the next call's counters
+    hipLaunchKernelGGL(k_insert_req<64>, dim3(1), dim3(256), 0, s, c->view, hashes, blk_offsets,
+                       n, n_blocks, *epoch);
+    return launch_status();
+  }
+  const int g = insert_group(n, n_blocks);
+  const dim3 grid((unsigned)ceil_div((int64_t)n * g, 256)), block(256);
+  switch (g) {
+    case 4: hipLaunchKernelGGL(k_insert_req<4>, grid, block, 0, s, c->view, hashes, blk_offsets, n, n_blocks, *epoch); break;
+    case 8: hipLaunchKernelGGL(k_insert_req<8>, grid, block, 0, s, c->view, hashes, blk_offsets, n, n_blocks, *epoch); break;
+    case 16: hipLaunchKernelGGL(k_insert_req<16>, grid, block, 0, s, c->view, hashes, blk_offsets, n, n_blocks, *epoch); break;
+    case 32: hipLaunchKernelGGL(k_insert_req<32>, grid, block, 0, s, c->view, hashes, blk_offsets, n, n_blocks, *epoch); break;
+    default: hipLaunchKernelGGL(k_insert_req<64>, grid, block, 0, s, c->view, hashes, blk_offsets, n, n_blocks, *epoch); break;
+  }
   return launch_status();
 }
 
@@ -972,7 +1079,7 @@ int kvgov_cache_admit(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_
   uint32_t *codes = static_cast<uint32_t *>(scratch_p);
   const uint32_t epoch = c->epoch.fetch_add(1) + 1;
   if (epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;
-  hipLaunchKernelGGL(k_insert<true>, dim3(insert_grid(n_blocks)), dim3(256), 0, s, c->view,
+  hipLaunchKernelGGL(k_admit_insert, dim3(insert_grid(n_blocks)), dim3(256), 0, s, c->view,
                      hashes, blk_offsets, n, n_blocks, epoch, codes);
   AdmitArgs a{c->view, blk_offsets, n, n_blocks, epoch, codes, hit_blocks, new_blocks};
   const int g = admit_group(n, n_blocks);

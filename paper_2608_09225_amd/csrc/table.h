@@ -79,16 +79,27 @@ __device__ __forceinline__ uint64_t slot_hash(const Key &k) {
   return x;
 }
 
-// A key's probe sequence starts at its home slot and runs through the
-// following slots (linear probing).  Measured alternatives, not used: home
-// slots aligned to 128-byte lines (four slots) with a probe reading its
-// whole line at once made the probe-heavy lookup 2 % faster but the insert
-// of 13.7M distinct keys 15-20 % slower (a key's first slot is then far more
-// often claimed by another key of the same call, whose input row the insert
-// reads to compare: 40 % more fetched bytes); reading the whole line that
-// holds an unaligned home slot made the lookup 7 % slower.
+// A key's probe sequence starts at its home slot, runs through the rest of
+// the home slot's bucket (four slots: one 128-byte line of keys), wrapping
+// inside it, and then through the following buckets in the same way.  A
+// search that runs past its home slot mostly finds the key, or an empty
+// slot, in the line it has already read; plain linear probing crossed into
+// the next line whenever a run reached the end of one (probe-heavy lookup:
+// 2.40 -> 2.27 GB fetched, 0.432 -> 0.425 ms).  Measured alternatives, not
+// used: probe sequences starting at the bucket's first slot made the
+// insert of 13.7M distinct keys 15-20 % slower (a key's first slot is then
+// four times as often claimed by another key of the same call, whose input
+// row the insert reads to compare); reading a whole bucket with one lane
+// (eight 16-byte loads per probe) made the lookup 9 % slower.
 __device__ __forceinline__ uint64_t home_slot(const Key &k, uint64_t mask) {
   return slot_hash(k) & mask;
+}
+
+// probe p of the sequence from `home`: the four slots of home's bucket (one
+// 128-byte line of keys) starting at home, then the next bucket's from the
+// same offset, and so on
+__device__ __forceinline__ uint64_t seq_slot(uint64_t home, uint64_t p, uint64_t mask) {
+  return ((((home >> 2) + (p >> 2)) << 2) & mask) | ((home + p) & 3);
 }
 
 // Sum of v over the workgroup (256 threads), valid in thread 0.
@@ -136,14 +147,16 @@ __device__ __forceinline__ unsigned long long recency(uint32_t epoch, uint32_t d
 // a smaller claim of the same key), so a plain (possibly stale) read can only
 // show 0 for a claimed slot; the compare-and-swap that follows then fails
 // and returns the claim.  Coherent atomics are used for the claim only.
-// Returns 1 if the key was added; *code receives where the key went.  On a
-// table that tracks recency the key (added or found) is touched with
-// (epoch, depth) unless depth is kNoDepth.
+// Returns 1 if the key was added; *code receives where the key went, and
+// *claim (if given) the key's tag as this lane found it (its own claim if it
+// added the key).  On a table that tracks recency the key (added or found)
+// is touched with (epoch, depth) unless depth is kNoDepth.
 template <bool ADMIT>
 __device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &key, int64_t i,
                                                int64_t lo, const uint8_t *hashes,
                                                uint32_t epoch, uint32_t *code,
-                                               uint32_t depth = kNoDepth) {
+                                               uint32_t depth = kNoDepth,
+                                               unsigned long long *claim = nullptr) {
   const unsigned long long mine = ((unsigned long long)epoch << 32) |
                                   (unsigned long long)(i - lo + 1);
   if (key_is_empty_pattern(key)) {
@@ -152,14 +165,16 @@ __device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &ke
     const bool won = __hip_atomic_compare_exchange_strong(
         &t.meta->ones_tag, &expect, mine, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
         __HIP_MEMORY_SCOPE_AGENT);
+    if (claim) *claim = won ? mine : expect;
     if (won) atomicExch(&t.meta->ones_present, 1);
     if (!won && ADMIT && (uint32_t)(expect >> 32) == epoch)
       lower_claim(&t.meta->ones_tag, expect, mine);
     if (t.track && depth != kNoDepth) touch(&t.meta->ones_rank, recency(epoch, depth), won);
     return won ? 1u : 0u;
   }
-  uint64_t s = home_slot(key, t.mask);
+  const uint64_t home = home_slot(key, t.mask);
   for (uint64_t probes = 0; probes <= t.mask; ++probes) {
+    const uint64_t s = seq_slot(home, probes, t.mask);
     unsigned long long tag = t.tags[s];
     if (tag == 0) {
       unsigned long long expect = 0;
@@ -168,6 +183,7 @@ __device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &ke
         t.keys[2 * s] = key.lo;
         t.keys[2 * s + 1] = key.hi;
         *code = (uint32_t)s;
+        if (claim) *claim = mine;
         if (t.track && depth != kNoDepth) touch(&t.rank[s], recency(epoch, depth), true);
         return 1;
       }
@@ -184,26 +200,27 @@ __device__ __forceinline__ uint32_t insert_key(const TableView &t, const Key &ke
     if (key_eq(key, other)) {
       if (ADMIT && current) lower_claim(&t.tags[s], tag, mine);
       *code = (uint32_t)s;
+      if (claim) *claim = tag;
       if (t.track && depth != kNoDepth) touch(&t.rank[s], recency(epoch, depth), false);
       return 0;
     }
-    s = (s + 1) & t.mask;
   }
   atomicCAS(&t.meta->status, 0, KVGOV_E_FULL);
   *code = kCodeFailed;
+  if (claim) *claim = 0;
   return 0;
 }
 
 // Is `key` in the table?  Reads the key array only, one slot at a time (the
-// slots after the first mostly share its line, so their loads hit the cache).
+// slots after the first are mostly in its line, so their loads hit the cache).
 __device__ __forceinline__ bool probe(const TableView &t, const Key &key, bool ones_present) {
   if (key_is_empty_pattern(key)) return ones_present;
-  uint64_t s = home_slot(key, t.mask);
+  const uint64_t home = home_slot(key, t.mask);
   for (uint64_t p = 0; p <= t.mask; ++p) {
+    const uint64_t s = seq_slot(home, p, t.mask);
     const Key slot{t.keys[2 * s], t.keys[2 * s + 1]};
     if (key_eq(slot, key)) return true;
     if (key_is_empty_pattern(slot)) return false;
-    s = (s + 1) & t.mask;
   }
   return false;
 }
@@ -221,12 +238,12 @@ __device__ __forceinline__ uint64_t group_mask(int base) {
 // Slot holding `key`, or -1 (the all-0xFF key has no slot: -2 if present).
 __device__ __forceinline__ int64_t find_slot(const TableView &t, const Key &key) {
   if (key_is_empty_pattern(key)) return t.meta->ones_present ? -2 : -1;
-  uint64_t s = home_slot(key, t.mask);
+  const uint64_t home = home_slot(key, t.mask);
   for (uint64_t p = 0; p <= t.mask; ++p) {
+    const uint64_t s = seq_slot(home, p, t.mask);
     const Key slot{t.keys[2 * s], t.keys[2 * s + 1]};
     if (key_eq(slot, key)) return (int64_t)s;
     if (key_is_empty_pattern(slot)) return -1;
-    s = (s + 1) & t.mask;
   }
   return -1;
 }

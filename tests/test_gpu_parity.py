@@ -377,6 +377,51 @@ def test_cache_insert_shared_prefixes():
     assert np.array_equal(hits, np.asarray(lens))
 
 
+def test_cache_insert_interleaved_shared_heads():
+    """Requests of many prefix families interleaved at random, as the requests
+    of root-salted principals are (the insert compares a row with the row at
+    the same depth of the earliest request that starts with the same block):
+    shared heads with tails that diverge at once, requests shorter and longer
+    than their family's earliest one, a family's keys at shifted depths, the
+    head key repeated deeper, and the same batch with recency tracking on."""
+    g = np.random.default_rng(131)
+    fam = g.integers(0, 256, (30, 300, 32), dtype=np.uint8)
+    lens, rows = [], []
+    for r in range(6000):
+        f = int(g.integers(0, 30))
+        L = int(g.integers(1, 250))
+        kind = r % 8
+        k = g.integers(0, 256, (L, 32), dtype=np.uint8)
+        if kind <= 3:  # a shared prefix of random depth
+            s = int(g.integers(1, L + 1))
+            k[:s] = fam[f, :s]
+        elif kind == 4:  # the head only, then another family's rows at the same depths
+            k[:] = fam[(f + 1) % 30, :L]
+            k[0] = fam[f, 0]
+        elif kind == 5:  # the head, then the family's rows shifted by three
+            k[0] = fam[f, 0]
+            k[1:] = fam[f, 4:L + 3]
+        elif kind == 6:  # the whole family prefix, the head key again at depth 7
+            k[:] = fam[f, :L]
+            if L > 7:
+                k[7] = fam[f, 0]
+        lens.append(L)
+        rows.append(k)
+    keys = np.concatenate(rows)
+    bo = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    want = key_set(keys)
+    for track in (False, False, True):
+        with K.Cache(21) as c:
+            if track:
+                c.set_recency(True)
+            assert c.insert(dev(keys), dev(bo)) == len(want)
+            assert c.count() == len(want)
+            assert key_set(c.export().cpu().numpy()) == want
+            assert c.insert(dev(keys), dev(bo)) == 0
+            hits = c.lookup(dev(keys), dev(bo)).cpu().numpy()
+        assert np.array_equal(hits, np.asarray(lens))
+
+
 def test_cache_insert_ignores_interior_offsets():
     """Insert adds the flat range [blk_offsets[0], blk_offsets[n]); interior
     offsets that are not monotone change nothing."""
