@@ -260,7 +260,8 @@ def admit_bytes(n_req: int, rows: int, n_new: int) -> int:
 
 
 def admit_group(n: int, rows: int) -> int:
-    """Lanes per request of the admission scan (the library's rule)."""
+    """Lanes per request of the admission scan, the plain insert and the radix
+    edge walk (the library's rule)."""
     avg = rows // n if n else 0
     g = 4
     while g < 64 and g * 2 < avg:
@@ -1136,9 +1137,9 @@ def run_workload(name: str, args, dev, K, torch):
     }
     if admission:
         atr = [recorded_traffic(k, wl.name, "cache")
-               for k in ("k_insert<true>", f"k_admit_scan<{admit_group(X.n, nX)}>")]
+               for k in ("k_admit_insert", f"k_admit_scan<{admit_group(X.n, nX)}>")]
         roof_lookup = {
-            "bound": "hbm", "kernel": "k_insert<true> + k_admit_scan (kvgov_cache_admit)",
+            "bound": "hbm", "kernel": "k_admit_insert + k_admit_scan (kvgov_cache_admit)",
             "achieved": look_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": look_gbs / HBM_PEAK_GBS,
             "traffic": None if None in atr else sum(t["bytes"] for t in atr),
@@ -1344,10 +1345,10 @@ def run_workload(name: str, args, dev, K, torch):
                                  for m in modes]))
         g_i = admit_group(A.n, nA)
         itr = [recorded_traffic(k, wl.name, t) for k, t in
-               (("k_radix_roots", "radix"), ("k_insert<false>", "cache"),
+               (("k_radix_roots", "radix"), (f"k_insert_req<{g_i}>", "cache"),
                 (f"k_radix_edges<{g_i}>", "radix"))]
         result["roofline_radix_insert"] = {
-            "bound": "hbm", "kernel": f"k_radix_roots + k_insert + k_radix_edges<{g_i}> "
+            "bound": "hbm", "kernel": f"k_radix_roots + k_insert_req<{g_i}> + k_radix_edges<{g_i}> "
                                       "(kvgov_radix_insert)",
             "achieved": ins_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": ins_gbs / HBM_PEAK_GBS,
@@ -1370,11 +1371,13 @@ def run_workload(name: str, args, dev, K, torch):
         }
     if not probe_only and not admission and not radix_cfg:
         ins_gbs = float(np.mean([phases[W.MODE_NAMES[m]]["insert"]["gbs"] for m in modes]))
-        itr = recorded_traffic("k_insert<false>", wl.name, "cache")
+        g_ins = admit_group(A.n, nA)
+        itr = recorded_traffic(f"k_insert_req<{g_ins}>", wl.name, "cache")
         ins_s = float(np.mean([phases[W.MODE_NAMES[m]]["insert"]["ms_median"]
                                for m in modes])) / 1e3
         result["roofline_insert"] = {
-            "bound": "hbm", "kernel": "k_insert (set-union insert)", "achieved": ins_gbs,
+            "bound": "hbm", "kernel": f"k_insert_req<{g_ins}> (set-union insert)",
+            "achieved": ins_gbs,
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ins_gbs / HBM_PEAK_GBS,
             "traffic": None if itr is None else itr["bytes"],
             "traffic_frac": None if itr is None else itr["bytes"] / ins_s / 1e9 / HBM_PEAK_GBS,
