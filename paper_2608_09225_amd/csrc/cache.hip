@@ -74,7 +74,7 @@ __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long l
     keys[2 * s] = ones;
     keys[2 * s + 1] = ones;
     tags[s] = 0;
-    rank[s] = 0;
+    if (rank) rank[s] = 0;
   }
 }
 
@@ -811,9 +811,15 @@ unsigned grid_for(int64_t work, int per_cu) {
   return (unsigned)std::max<int64_t>(1, std::min<int64_t>(ceil_div(work, 256), cap));
 }
 
+// The recency words are rewritten only if something may have written them
+// since they were last cleared (a tracked insert or admission, an eviction,
+// an erasure): on a table that never tracks, a clear writes 40 of its 48
+// bytes per slot.
 int enqueue_clear(kvgov_cache *c, hipStream_t s) {
   hipLaunchKernelGGL(k_cache_fill, dim3(grid_for(c->slots, 64)), dim3(256), 0, s, c->view.keys,
-                     c->view.tags, c->view.rank, c->slots, c->view.meta);
+                     c->view.tags, c->rank_dirty ? c->view.rank : nullptr, c->slots,
+                     c->view.meta);
+  c->rank_dirty = false;
   c->epoch.store(0);
   return launch_status();
 }
@@ -922,6 +928,7 @@ int kvgov::cache_insert_rows(kvgov_cache *c, const uint8_t *hashes, const int64_
                              int32_t n, int64_t n_blocks, hipStream_t s, uint32_t *epoch) {
   *epoch = c->epoch.fetch_add(1) + 1;
   if (*epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;  // 2^32 - 1 inserts since clear
+  if (c->view.track) c->rank_dirty = true;
   if (n == 0) {
     // no request: only the batch check and the next call's counters
     hipLaunchKernelGGL(k_insert_req<64>, dim3(1), dim3(256), 0, s, c->view, hashes, blk_offsets,
@@ -1079,6 +1086,7 @@ int kvgov_cache_admit(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_
   uint32_t *codes = static_cast<uint32_t *>(scratch_p);
   const uint32_t epoch = c->epoch.fetch_add(1) + 1;
   if (epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;
+  if (c->view.track) c->rank_dirty = true;
   hipLaunchKernelGGL(k_admit_insert, dim3(insert_grid(n_blocks)), dim3(256), 0, s, c->view,
                      hashes, blk_offsets, n, n_blocks, epoch, codes);
   AdmitArgs a{c->view, blk_offsets, n, n_blocks, epoch, codes, hit_blocks, new_blocks};
@@ -1125,6 +1133,7 @@ int kvgov_cache_evict(kvgov_cache *c, int64_t max_keys, int64_t *n_kept, void *s
                        m.hist);
     hipLaunchKernelGGL(k_rank_select, dim3(1), dim3(kRankBins), 0, s, m.st, m.hist);
   }
+  c->rank_dirty = true;
   return compact_rebuild(c, s, m, &m.st->kept, n_kept);
 }
 
@@ -1142,6 +1151,7 @@ int kvgov_cache_erase(kvgov_cache *c, const uint8_t *keys, int64_t n_keys, int64
   if (n_keys > 0)
     hipLaunchKernelGGL(k_erase_mark, dim3((unsigned)ceil_div(n_keys, 256)), dim3(256), 0, s,
                        c->view, keys, n_keys, m.st);
+  c->rank_dirty = true;
   return compact_rebuild(c, s, m, &m.st->erased, n_erased);
 }
 

@@ -263,5 +263,8 @@ struct kvgov_cache {
   int64_t slots;
   kvgov::TableView view;  // view.track: recency tracking on
   std::atomic<uint32_t> epoch;
+  // recency words may be nonzero (set when a call that can write them is
+  // enqueued; the next clear rewrites them)
+  std::atomic<bool> rank_dirty{true};
 };
 

@@ -203,3 +203,36 @@ def test_untracked_keys_in_a_sparse_table(keep):
         assert c.evict(max_keys) == T.evict(max_keys)
         assert key_set(c.export()) == T.keys
     assert len(T.keys) == (8 if keep == "all" else 5)
+
+
+def test_clear_resets_recency_of_a_tracked_table():
+    """A clear skips the recency words unless a call since the last clear may
+    have written them.  Keys ranked by tracked inserts (stamps up to 5), a
+    clear, the same keys again untracked and other keys tracked (stamps 1
+    and 2): the untracked keys must rank lowest, as if the table were new."""
+    a = arr([key_of(3000 + i) for i in range(3)])
+    b = arr([key_of(4000 + i) for i in range(5)])
+    bo_a = np.array([0, 3], np.int64)
+    bo_b = np.array([0, 5], np.int64)
+    T = O.Table()
+    T.keys |= {a[i].tobytes() for i in range(3)}  # untracked after the clear
+    T.insert(b, bo_b)
+    with KV.Cache(16) as c:
+        c.set_recency(True)
+        for _ in range(5):
+            c.insert(dev(a), dev(bo_a))
+        c.clear()
+        c.set_recency(False)
+        c.insert(dev(a), dev(bo_a))
+        c.set_recency(True)
+        c.insert(dev(b), dev(bo_b))
+        assert c.evict(5) == T.evict(5)
+        assert key_set(c.export()) == T.keys == {b[i].tobytes() for i in range(5)}
+        # a table that never tracked: clears skip the words, erasure still exact
+    with KV.Cache(12) as c:
+        for _ in range(2):
+            c.insert(dev(a), dev(bo_a))
+            assert c.erase(dev(a[:1])) == 1
+            assert key_set(c.export()) == {a[i].tobytes() for i in (1, 2)}
+            c.clear()
+            assert c.count() == 0
