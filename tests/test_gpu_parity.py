@@ -422,6 +422,37 @@ def test_cache_insert_interleaved_shared_heads():
         assert np.array_equal(hits, np.asarray(lens))
 
 
+@pytest.mark.parametrize("max_len", [3, 20, 40])
+def test_cache_insert_shared_heads_short_requests(max_len):
+    """Short requests (few lanes per request: 4, 8, 16) of interleaved
+    families whose first keys repeat, with the all-zero and all-0xFF keys as
+    first keys of some families, empty requests between them, and rows
+    that equal an earlier family member's at the same depth only sometimes."""
+    g = np.random.default_rng(141 + max_len)
+    fam = g.integers(0, 256, (12, max_len, 32), dtype=np.uint8)
+    fam[0, 0] = 0
+    fam[1, 0] = 255
+    lens, rows = [], []
+    for r in range(20000):
+        L = int(g.integers(0, max_len + 1))
+        f = int(g.integers(0, 12))
+        k = g.integers(0, 256, (L, 32), dtype=np.uint8)
+        if L:
+            s_ = int(g.integers(1, L + 1))
+            k[:s_] = fam[f, :s_]
+        lens.append(L)
+        rows.append(k)
+    keys = np.concatenate(rows)
+    bo = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    want = key_set(keys)
+    with K.Cache(20) as c:
+        assert c.insert(dev(keys), dev(bo)) == len(want)
+        assert c.count() == len(want)
+        assert key_set(c.export().cpu().numpy()) == want
+        hits = c.lookup(dev(keys), dev(bo)).cpu().numpy()
+    assert np.array_equal(hits, np.asarray(lens))
+
+
 def test_cache_insert_ignores_interior_offsets():
     """Insert adds the flat range [blk_offsets[0], blk_offsets[n]); interior
     offsets that are not monotone change nothing."""
