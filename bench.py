@@ -1211,7 +1211,10 @@ def run_workload(name: str, args, dev, K, torch):
         # fits in two 64-request workgroups per CU, else the mixed kernel
         # (longest requests on lane-pair workgroups, the rest one lane each)
         kname = "k_chains_lp" if X.n <= 2 * 64 * cus else "k_chains_mixed"
-        tr = {m: recorded_traffic(f"{kname}<{m}>", wl.name, "chains") for m in modes}
+        # the lane-pair kernel's second template argument: a fourth wave
+        # sharing the schedule (one workgroup per CU) or not (two per CU)
+        pair = "" if kname == "k_chains_mixed" else (",true" if X.n <= 64 * cus else ",false")
+        tr = {m: recorded_traffic(f"{kname}<{m}{pair}>", wl.name, "chains") for m in modes}
         traffic = None
         if all(t is not None for t in tr.values()):
             traffic = float(np.mean([t["bytes"] for t in tr.values()]))
