@@ -50,6 +50,41 @@ def build_one(name: str, sources, verbose: bool = False) -> str:
     return out
 
 
+# Host-side AddressSanitizer build of libkvgov (the device code is built as
+# usual; only the host validation and bookkeeping are instrumented).  The
+# process that loads it must preload the ASan runtime (asan_runtime()).
+ASAN_FLAGS = [
+    "-O1", "-g",
+    "-Xarch_host", "-fsanitize=address",
+    "-Xarch_host", "-fno-omit-frame-pointer",
+    "-shared-libasan",
+]
+
+
+def build_host_asan(out_dir: str) -> str:
+    """Builds libkvgov with host AddressSanitizer into out_dir; returns its path."""
+    out = os.path.join(out_dir, "libkvgov_host_asan.so")
+    flags = [f for f in FLAGS if f != "-O3"] + ASAN_FLAGS
+    cmd = [hipcc(), *flags, "-o", out, *[os.path.join(HERE, s) for s in LIBS["libkvgov.so"]]]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{' '.join(cmd)}\n{res.stderr}")
+    return out
+
+
+def asan_runtime() -> str:
+    """Path of the shared ASan runtime of hipcc's clang, or '' if absent."""
+    clang = os.path.join(os.path.dirname(os.path.realpath(hipcc())), "..", "llvm", "bin", "clang")
+    for c in (clang, "/opt/rocm/llvm/bin/clang"):
+        if os.path.exists(c):
+            res = subprocess.run([c, "-print-file-name=libclang_rt.asan-x86_64.so"],
+                                 capture_output=True, text=True)
+            path = res.stdout.strip()
+            if res.returncode == 0 and os.path.isabs(path) and os.path.exists(path):
+                return path
+    return ""
+
+
 def build(verbose: bool = False) -> str:
     """Builds every library; returns the path of libkvgov.so."""
     for name, sources in LIBS.items():
