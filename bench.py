@@ -1137,9 +1137,9 @@ def run_workload(name: str, args, dev, K, torch):
     }
     if admission:
         atr = [recorded_traffic(k, wl.name, "cache")
-               for k in ("k_admit_insert", f"k_admit_scan<{admit_group(X.n, nX)}>")]
+               for k in ("k_chunk_insert<true>", f"k_admit_scan<{admit_group(X.n, nX)}>")]
         roof_lookup = {
-            "bound": "hbm", "kernel": "k_admit_insert + k_admit_scan (kvgov_cache_admit)",
+            "bound": "hbm", "kernel": "k_chunk_insert<true> + k_admit_scan (kvgov_cache_admit)",
             "achieved": look_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": look_gbs / HBM_PEAK_GBS,
             "traffic": None if None in atr else sum(t["bytes"] for t in atr),

@@ -78,7 +78,7 @@ __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long l
   }
 }
 
-// Consecutive keys per wave chunk of the admission insert.  Longer chunks mean fewer
+// Consecutive keys per wave chunk of k_chunk_insert.  Longer chunks mean fewer
 // waves in flight at once, so that the copies of a key that many requests
 // hold (a principal's shared prefix) reach its slot over a longer span and
 // most of them find it claimed by a plain read instead of racing for it
@@ -86,7 +86,7 @@ __global__ __launch_bounds__(256) void k_cache_fill(u32x4 *keys, unsigned long l
 constexpr int kInsChunk = 256;
 
 // The largest r in [0, n) with bo[r] <= f (bo non-decreasing in a valid
-// batch; any answer in range is harmless otherwise, see k_admit_insert).  Every
+// batch; any answer in range is harmless otherwise, see k_chunk_insert).  Every
 // lane of a wave searches the same f.
 __device__ __forceinline__ int32_t find_request(const int64_t *bo, int32_t n, int64_t f) {
   int32_t a = 0, b = n - 1;
@@ -97,18 +97,17 @@ __device__ __forceinline__ int32_t find_request(const int64_t *bo, int32_t n, in
   return a;
 }
 
-// First half of the admission: the insert of the batch's rows, with claims
-// lowered to the earliest row, and codes[f] recording where row f's key went
-// (kCodeDup for a key skipped as equal to the previous request's, which is
-// in an earlier request by construction).  A wave takes chunks of kInsChunk
-// consecutive rows, 64 at a time.  Before touching the table a key is
-// compared with the key at the same block position of the previous request
-// (requests that share a prefix - the same principal, or any principal
-// below the boundary block - hold the same keys there): an equal earlier
-// key makes this one a duplicate that needs no table access, so a prefix
-// shared by thousands of requests costs a few table operations per key
-// instead of thousands of atomics on one slot.  The request of each key
-// comes from a window of 64 request starts (a search over lanes); the
+// Insert walking the batch in chunks of kInsChunk consecutive rows per wave,
+// 64 at a time: the admission's first half (ADMIT), and the plain insert of
+// batches whose requests are so long that a group per request would leave
+// the chip idle (a flat key set given as one request).  Before touching the
+// table a key is compared with the key at the same block position of the
+// previous request (requests that share a prefix - the same principal, or
+// any principal below the boundary block - hold the same keys there): an
+// equal earlier key makes this one a duplicate that needs no table access,
+// so a prefix shared by thousands of requests costs a few table operations
+// per key instead of thousands of atomics on one slot.  The request of each
+// key comes from a window of 64 request starts (a search over lanes); the
 // comparison is only an optimisation: skipping a key that equals an
 // earlier key of the batch is always correct (the earlier one is inserted,
 // or is itself a duplicate of an earlier one), and the compared position
@@ -116,7 +115,12 @@ __device__ __forceinline__ int32_t find_request(const int64_t *bo, int32_t n, in
 // cause a wrong result or an out-of-range read.  A row's request, and so
 // its depth (its position in the request, which the recency rank holds),
 // is exact: rows whose request lies past the window search for it.
-__global__ __launch_bounds__(256) void k_admit_insert(TableView t, const uint8_t *hashes,
+//
+// ADMIT: claims are lowered to the earliest row, and codes[f] records where
+// row f's key went (kCodeDup for a key skipped as equal to the previous
+// request's, which is in an earlier request by construction).
+template <bool ADMIT>
+__global__ __launch_bounds__(256) void k_chunk_insert(TableView t, const uint8_t *hashes,
                                                       const int64_t *blk_offsets, int32_t n,
                                                       int64_t n_blocks, uint32_t epoch,
                                                       uint32_t *codes) {
@@ -174,8 +178,8 @@ __global__ __launch_bounds__(256) void k_admit_insert(TableView t, const uint8_t
         // the depth of the key: its row within its request (clamped; only
         // malformed interior offsets put it outside [0, 2^31))
         const uint32_t depth = (uint32_t)(jj < 0 ? 0 : (jj > 0x7FFFFFFF ? 0x7FFFFFFF : jj));
-        if (!dup) added += insert_key<true>(t, key, f, lo, hashes, epoch, &code, depth);
-        codes[f] = code;
+        if (!dup) added += insert_key<ADMIT>(t, key, f, lo, hashes, epoch, &code, depth);
+        if (ADMIT) codes[f] = code;
       }
       rc = __shfl(r, 63, 64);
     }
@@ -329,7 +333,7 @@ struct AdmitArgs {
   int32_t n;
   int64_t n_blocks;
   uint32_t epoch;
-  const uint32_t *codes;  // per row, from k_admit_insert
+  const uint32_t *codes;  // per row, from k_chunk_insert<true>
   int32_t *hit_blocks;
   int32_t *new_blocks;
 };
@@ -341,7 +345,7 @@ struct AdmitArgs {
 //                      before b0 (an earlier request holds it);
 //   new for r     <=>  K's earliest row is f itself.
 // hit_blocks[r] = first row not visible (relative to b0), new_blocks[r] =
-// rows new for r.  The earliest rows are final: k_admit_insert has ended.
+// rows new for r.  The earliest rows are final: k_chunk_insert<true> has ended.
 template <int G>
 __global__ __launch_bounds__(256) void k_admit_scan(AdmitArgs a) {
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -353,7 +357,7 @@ __global__ __launch_bounds__(256) void k_admit_scan(AdmitArgs a) {
   const uint64_t gmask = group_mask<G>(base);
   const int64_t lo = a.blk_offsets[0], hi = a.blk_offsets[a.n];
   const int64_t b0 = a.blk_offsets[r], b1 = a.blk_offsets[r + 1];
-  // the batch check of k_admit_insert (which then wrote no codes), and this
+  // the batch check of k_chunk_insert<true> (which then wrote no codes), and this
   // request's rows inside the batch
   if (lo < 0 || hi < lo || hi > a.n_blocks || hi - lo >= 0xFFFFFFFFll || b0 < lo || b1 < b0 ||
       b1 > hi) {
@@ -824,6 +828,12 @@ int enqueue_clear(kvgov_cache *c, hipStream_t s) {
   return launch_status();
 }
 
+// The plain insert takes a group of lanes per request while requests
+// average at most this many rows (a group walks its request 64 rows at a
+// time, so one request of 2^20 rows would take 16k steps of one wave), and
+// the chunked walk above it.
+constexpr int64_t kReqInsertMaxAvg = 4096;
+
 // Lanes per request of the plain insert: about one lane per two rows of
 // the average request, 4 to 64.
 int insert_group(int32_t n, int64_t n_blocks) {
@@ -833,7 +843,7 @@ int insert_group(int32_t n, int64_t n_blocks) {
   return g;
 }
 
-// Admission insert: waves of 4 x kInsChunk keys, at most 16 workgroups per CU.
+// k_chunk_insert: waves of 4 x kInsChunk keys, at most 16 workgroups per CU.
 unsigned insert_grid(int64_t n_blocks) {
   const int64_t groups = ceil_div(std::max<int64_t>(n_blocks, 1), (int64_t)kInsChunk * 4);
   return (unsigned)std::min<int64_t>(groups, (int64_t)device_cu_count() * 16);
@@ -933,6 +943,12 @@ int kvgov::cache_insert_rows(kvgov_cache *c, const uint8_t *hashes, const int64_
     // no request: only the batch check and the next call's counters
     hipLaunchKernelGGL(k_insert_req<64>, dim3(1), dim3(256), 0, s, c->view, hashes, blk_offsets,
                        n, n_blocks, *epoch);
+    return launch_status();
+  }
+  if (n_blocks > (int64_t)n * kReqInsertMaxAvg) {
+    // few, long requests: a group per request would leave the chip idle
+    hipLaunchKernelGGL(k_chunk_insert<false>, dim3(insert_grid(n_blocks)), dim3(256), 0, s,
+                       c->view, hashes, blk_offsets, n, n_blocks, *epoch, nullptr);
     return launch_status();
   }
   const int g = insert_group(n, n_blocks);
@@ -1087,8 +1103,8 @@ int kvgov_cache_admit(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_
   const uint32_t epoch = c->epoch.fetch_add(1) + 1;
   if (epoch == 0xFFFFFFFFu) return KVGOV_E_UNSUPPORTED;
   if (c->view.track) c->rank_dirty = true;
-  hipLaunchKernelGGL(k_admit_insert, dim3(insert_grid(n_blocks)), dim3(256), 0, s, c->view,
-                     hashes, blk_offsets, n, n_blocks, epoch, codes);
+  hipLaunchKernelGGL(k_chunk_insert<true>, dim3(insert_grid(n_blocks)), dim3(256), 0, s,
+                     c->view, hashes, blk_offsets, n, n_blocks, epoch, codes);
   AdmitArgs a{c->view, blk_offsets, n, n_blocks, epoch, codes, hit_blocks, new_blocks};
   const int g = admit_group(n, n_blocks);
   const dim3 grid((unsigned)ceil_div((int64_t)n * g, 256)), block(256);

@@ -453,17 +453,44 @@ def test_cache_insert_shared_heads_short_requests(max_len):
     assert np.array_equal(hits, np.asarray(lens))
 
 
-def test_cache_insert_ignores_interior_offsets():
+@pytest.mark.parametrize("scale", [1, 10])
+def test_cache_insert_ignores_interior_offsets(scale):
     """Insert adds the flat range [blk_offsets[0], blk_offsets[n]); interior
-    offsets that are not monotone change nothing."""
+    offsets that are not monotone change nothing.  At scale 10 the requests
+    average over 4096 rows, which the insert walks in chunks of rows instead
+    of a group of lanes per request."""
     g = np.random.default_rng(121)
-    uniq = g.integers(0, 256, (500, 32), dtype=np.uint8)
-    keys = uniq[g.integers(0, 500, 9000)]
-    keys[4000:4500] = keys[3000:3500]  # a repeated stretch
-    bo = np.array([0, 5000, 100, 7000, 20, 8999, 3, 9000], np.int64)
-    with K.Cache(12) as c:
+    uniq = g.integers(0, 256, (500 * scale, 32), dtype=np.uint8)
+    keys = uniq[g.integers(0, 500 * scale, 9000 * scale)]
+    keys[4000 * scale:4500 * scale] = keys[3000 * scale:3500 * scale]  # a repeated stretch
+    bo = np.array([0, 5000, 100, 7000, 20, 8999, 3, 9000], np.int64) * scale
+    with K.Cache(12 + scale // 5) as c:
         assert c.insert(dev(keys), dev(bo)) == len(key_set(keys))
         assert key_set(c.export().cpu().numpy()) == key_set(keys)
+
+
+def test_cache_insert_few_long_requests_with_shared_prefixes():
+    """Requests of tens of thousands of rows (the chunked walk), sharing
+    prefixes with their neighbours, then the same batch as short requests
+    (a group of lanes per request): the same key set either way."""
+    g = np.random.default_rng(151)
+    base = g.integers(0, 256, (30000, 32), dtype=np.uint8)
+    rows, lens = [], []
+    for r in range(6):
+        s_ = int(g.integers(0, 30000))
+        k = g.integers(0, 256, (30000, 32), dtype=np.uint8)
+        k[:s_] = base[:s_]
+        rows.append(k)
+        lens.append(30000)
+    keys = np.concatenate(rows)
+    want = key_set(keys)
+    for bo in (np.concatenate([[0], np.cumsum(lens)]).astype(np.int64),
+               np.arange(0, keys.shape[0] + 1, 100, dtype=np.int64)):
+        with K.Cache(20) as c:
+            assert c.insert(dev(keys), dev(bo)) == len(want)
+            assert key_set(c.export().cpu().numpy()) == want
+            hits = c.lookup(dev(keys), dev(bo)).cpu().numpy()
+        assert np.array_equal(hits, np.diff(bo))
 
 
 @pytest.mark.parametrize("n_req", [1, 7, 64, 3000, 5000, 20000, 300000])
