@@ -172,6 +172,32 @@ def test_chains_long_with_scattered_boundaries(mode):
     assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("n_req", [3000, 40000])
+def test_chains_permutation_invariance(n_req):
+    """A request's digests depend only on its own tokens, principal and
+    boundary, not on where it sits in the batch: the same batch permuted
+    (lane-pair launch at 3000 requests, longest-first ordered mixed launch at
+    40,000, where a request's rank decides its workgroup kind) gives every
+    request the same rows, and a request repeated at the other end of the
+    batch gets identical digests."""
+    g = np.random.default_rng(51 + n_req)
+    lens = g.integers(0, 500, n_req)
+    lens[g.integers(0, n_req, 20)] = g.integers(3000, 6000, 20)  # a few long chains
+    b = ragged(53 + n_req, lens, P=11)
+    perm = g.permutation(n_req)
+    perm[-1] = perm[0]  # request perm[0] twice: first and last
+    bp = b.subset(perm)
+    Kb, ids = secret(12, 11)
+    sd = K.salts(Kb, dev(ids))
+    bo, bop = b.blk_offsets(), bp.blk_offsets()
+    rows = np.concatenate([np.arange(bo[r], bo[r + 1]) for r in perm])
+    for mode in (W.ROOT, W.BOUNDARY):
+        h = gpu_chains(b, sd, mode).cpu().numpy()
+        hp = gpu_chains(bp, sd, mode).cpu().numpy()
+        assert np.array_equal(h[rows], hp)
+        assert np.array_equal(hp[bop[0]:bop[1]], hp[bop[-2]:bop[-1]])
+
+
 def test_chains_unaligned_token_offsets():
     """Requests starting at any token offset (tokens not 16-byte aligned)."""
     b = ragged(41, [1, 35, 2, 70, 3, 17, 5, 64])
@@ -236,6 +262,44 @@ def test_chains_invariants_on_gpu():
     bk = Batch(b.tokens, b.tok_offsets, b.principal, np.full(64, 100, np.int32))
     bnd = gpu_chains(bk, sd, W.BOUNDARY).cpu().numpy().reshape(64, 18, 32)
     assert np.array_equal(bnd[:, :6], none.reshape(64, 18, 32)[:, :6])
+
+
+def test_chains_principals_disjoint_on_gpu():
+    """The same token sequences under four principals: root salting gives
+    four disjoint key sets (no block of one principal's chains equals any
+    block of another's), boundary salting gives identical blocks below k
+    and disjoint ones from k on, and the unsalted chains coincide."""
+    g = np.random.default_rng(71)
+    base = ragged(73, g.integers(16, 900, 50))
+    n = base.n
+    idx = np.tile(np.arange(n), 4)
+    b = base.subset(idx)
+    b.principal[:] = np.repeat(np.arange(4, dtype=np.int32), n)
+    b.boundary_tok[:] = np.tile(base.boundary_tok, 4)
+    Kb, ids = secret(13, 4)
+    sd = K.salts(Kb, dev(ids))
+    bo = b.blk_offsets()
+    per = int(bo[n])  # rows of one principal's copy of the batch
+    none = gpu_chains(b, sd, W.NONE).cpu().numpy()
+    for p_ in range(1, 4):
+        assert np.array_equal(none[p_ * per:(p_ + 1) * per], none[:per])
+    root = gpu_chains(b, sd, W.ROOT).cpu().numpy()
+    sets = [key_set(root[p_ * per:(p_ + 1) * per]) for p_ in range(4)]
+    for p_ in range(4):
+        for q in range(p_ + 1, 4):
+            assert not (sets[p_] & sets[q])
+    bnd = gpu_chains(b, sd, W.BOUNDARY).cpu().numpy()
+    k = base.boundary_tok // 16
+    below = np.concatenate([np.arange(bo[r], bo[r] + min(int(k[r]), bo[r + 1] - bo[r]))
+                            for r in range(n)]).astype(np.int64)
+    above = np.setdiff1d(np.arange(per), below)
+    for p_ in range(1, 4):
+        assert np.array_equal(bnd[p_ * per + below], bnd[below])
+        assert np.array_equal(bnd[p_ * per + below], none[below])
+    upper = [key_set(bnd[p_ * per + above]) for p_ in range(4)]
+    for p_ in range(4):
+        for q in range(p_ + 1, 4):
+            assert not (upper[p_] & upper[q])
 
 
 # ---------------------------------------------------------------------------
