@@ -4,6 +4,9 @@ Every comparison is bit-exact (digests, hit counts, key sets, n_new): the
 path computes integers only.  Slot placement inside the table is not part of
 the contract and is never compared; the exported key *set* is.
 """
+import json
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -300,6 +303,65 @@ def test_chains_principals_disjoint_on_gpu():
     for p_ in range(4):
         for q in range(p_ + 1, 4):
             assert not (upper[p_] & upper[q])
+
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _gpu_cross_hit(pa, pb, mode, boundary, Kb, ids):
+    """Principal 0 caches prompt pa; principal 1 looks up pb: the hit blocks
+    of pb, through salts, chains, insert and lookup on the GPU."""
+    lens = np.array([pa.size, pb.size], np.int64)
+    b = Batch(np.concatenate([pa, pb]).astype(np.int32),
+              np.concatenate([[0], np.cumsum(lens)]).astype(np.int64),
+              np.array([0, 1], np.int32), np.array([boundary, boundary], np.int32))
+    hs = gpu_chains(b, K.salts(Kb, dev(ids)), mode)
+    bo = b.blk_offsets()
+    with K.Cache(12) as c:
+        c.insert(hs, dev(bo[:2]))
+        return int(c.lookup(hs, dev(bo[1:])).cpu().numpy()[0])
+
+
+def test_worked_examples_end_to_end():
+    """The paper's worked examples through the whole GPU path, against the
+    hit counts the paper prints or fixes (fixtures in tests/golden): a
+    prompt diverging from a cached 2119-token preamble at token 1990 keeps
+    124 blocks and at token 5 none (Sec. 5.6); another principal with the
+    same 2000- or 1500-token preamble hits 125 or 93 blocks unsalted and
+    with the salt at the boundary, and none with root salting (Sec. 4.2)."""
+    Kb, ids = secret(14, 2)
+    g = np.random.default_rng(81)
+    w1 = _golden("W1_divergence_position.json")
+    pre = g.integers(0, VOCAB, w1["preamble_tokens"], dtype=np.int32)
+    for mode in (W.NONE, W.ROOT):
+        for case in w1["cases"]:
+            probe = pre.copy()
+            i = case["diverge_at_token"]
+            probe[i] = (probe[i] + 1) % VOCAB
+            # both requests under principal 0 here: W1 is about one namespace
+            lens = np.array([pre.size, probe.size], np.int64)
+            b = Batch(np.concatenate([pre, probe]),
+                      np.concatenate([[0], np.cumsum(lens)]).astype(np.int64),
+                      np.zeros(2, np.int32), np.zeros(2, np.int32))
+            hs = gpu_chains(b, K.salts(Kb, dev(ids)), mode)
+            bo = b.blk_offsets()
+            with K.Cache(12) as c:
+                c.insert(hs, dev(bo[:2]))
+                hit = int(c.lookup(hs, dev(bo[1:])).cpu().numpy()[0])
+            assert hit == case["hit_blocks"], (mode, case)
+    for name in ("W2_boundary_preamble.json", "W3_short_preamble.json"):
+        w = _golden(name)
+        shared = g.integers(0, VOCAB, w["preamble_tokens"], dtype=np.int32)
+        pa = np.concatenate([shared, g.integers(0, VOCAB, w["tail_tokens"], dtype=np.int32)])
+        pb = np.concatenate([shared, g.integers(0, VOCAB, w["tail_tokens"], dtype=np.int32)])
+        for mname, mode in (("none", W.NONE), ("root", W.ROOT), ("boundary", W.BOUNDARY)):
+            hit = _gpu_cross_hit(pa, pb, mode, w["preamble_tokens"], Kb, ids)
+            assert hit == w["cross_principal_hit_blocks"][mname], (name, mname)
 
 
 # ---------------------------------------------------------------------------
