@@ -35,9 +35,9 @@
  *   - K and the salts are secrets: the library keeps no copy of K after
  *     kvgov_salts returns and logs nothing.
  *   - The calls allocate no device memory except kvgov_cache_create,
- *     kvgov_radix_create, the stream-ordered scratch of the maintenance
- *     calls (see there), and the per-stream scratch that kvgov_hash_chains
- *     and its resume variant, kvgov_cache_admit and the offset helpers use:
+ *     kvgov_radix_create, and the per-stream scratch that kvgov_hash_chains
+ *     and its resume variant, kvgov_cache_admit, the maintenance calls and
+ *     the offset helpers use:
  *     one buffer per (device, stream) the library has seen, grown on demand
  *     (growth waits for that stream, then frees the old buffer) and held
  *     until the process ends.  A stream runs its work in order, so its
@@ -349,10 +349,11 @@ int kvgov_cache_admit(kvgov_cache *c, const uint8_t *hashes, const int64_t *blk_
  * keep reading one key per probe), in stream order.  n_kept / n_erased: host
  * out or NULL; non-NULL waits for `stream`, stores the keys kept / the
  * distinct present keys erased, and returns any latched error.
- * Scratch: 40 * (slots + 1) bytes + 2 KiB from hipMallocAsync on `stream`,
- * freed in stream order.  Errors: KVGOV_E_INVAL, KVGOV_E_NOMEM,
+ * Scratch: 40 * (slots + 1) bytes + 2 KiB of the stream's scratch (see the
+ * notes at the top).  Errors: KVGOV_E_INVAL, KVGOV_E_NOMEM,
  * KVGOV_E_UNSUPPORTED (as above, or 2^32 - 1 calls since the last clear),
- * KVGOV_E_HIP, KVGOV_E_DEVICE.
+ * KVGOV_E_HIP, KVGOV_E_DEVICE; KVGOV_E_INTERNAL latched if the compaction
+ * counted more keys than the table's slots (never expected).
  */
 int kvgov_cache_set_recency(kvgov_cache *c, int32_t on);
 int kvgov_cache_evict(kvgov_cache *c, int64_t max_keys, int64_t *n_kept, void *stream);

@@ -756,9 +756,15 @@ __global__ __launch_bounds__(256) void k_rebuild_fill(TableView t) {
 __global__ __launch_bounds__(256) void k_reinsert(TableView t, const SelectState *st,
                                                   const uint8_t *keys,
                                                   const unsigned long long *rank,
-                                                  uint32_t epoch) {
+                                                  uint32_t epoch, int64_t cap) {
   __shared__ uint32_t lds4[4];
-  const int64_t n = (int64_t)st->kept;
+  int64_t n = (int64_t)st->kept;
+  if (n > cap) {
+    // more keys counted than the copy-out had room for (never expected: a
+    // table holds at most cap keys): reinsert the copies only
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicCAS(&t.meta->status, 0, KVGOV_E_INTERNAL);
+    n = cap;
+  }
   uint32_t added = 0;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * 256) {
@@ -857,15 +863,18 @@ int read_meta(kvgov_cache *c, CacheMeta *m, hipStream_t s) {
   return KVGOV_OK;
 }
 
-// Maintenance scratch, stream-ordered: selection state, the rank histogram
-// and room for every key of the table (32 B key + 8 B recency each).
+// Maintenance scratch, in the stream's scratch buffer: selection state, the
+// rank histogram and room for every key of the table (32 B key + 8 B recency
+// each).  `lk` holds the scratch registry while the call enqueues its
+// kernels; the stream runs its calls in order, so the buffer serves this
+// call until its kernels end.
 struct MaintScratch {
   SelectState *st = nullptr;
   unsigned int *hist = nullptr;
   u32x4 *keys = nullptr;
   unsigned long long *rank = nullptr;
-  void *base = nullptr;
   int64_t cap = 0;
+  std::unique_lock<std::mutex> lk;
 };
 
 // Workgroups of the compaction kernels: one step of 4096 slots each, at most
@@ -881,8 +890,10 @@ int maint_alloc(kvgov_cache *c, hipStream_t s, MaintScratch &m) {
   const size_t off_keys = off_hist + kRankBins * sizeof(unsigned int);
   const size_t off_rank = off_keys + (size_t)m.cap * 32;
   const size_t bytes = off_rank + (size_t)m.cap * 8;
-  if (hipMallocAsync(&m.base, bytes, s) != hipSuccess) return KVGOV_E_NOMEM;
-  uint8_t *b = static_cast<uint8_t *>(m.base);
+  void *base = nullptr;
+  const int rc = stream_scratch(s, bytes, &base, m.lk);
+  if (rc != KVGOV_OK) return rc;
+  uint8_t *b = static_cast<uint8_t *>(base);
   m.st = reinterpret_cast<SelectState *>(b);
   m.hist = reinterpret_cast<unsigned int *>(b + off_hist);
   m.keys = reinterpret_cast<u32x4 *>(b + off_keys);
@@ -892,7 +903,7 @@ int maint_alloc(kvgov_cache *c, hipStream_t s, MaintScratch &m) {
 
 // Copies out what ranks at or above the selected threshold, empties the
 // table and inserts the copies again; then reads one counter if asked
-// (waiting for the stream) and frees the scratch in stream order.
+// (waiting for the stream).
 int compact_rebuild(kvgov_cache *c, hipStream_t s, MaintScratch &m, const unsigned long long *count,
                     int64_t *out) {
   const uint32_t epoch = c->epoch.fetch_add(1) + 1;
@@ -902,14 +913,14 @@ int compact_rebuild(kvgov_cache *c, hipStream_t s, MaintScratch &m, const unsign
                        m.keys, m.rank, m.cap);
     hipLaunchKernelGGL(k_rebuild_fill, dim3(grid_for(c->slots, 64)), dim3(256), 0, s, c->view);
     hipLaunchKernelGGL(k_reinsert, dim3(grid_for(m.cap, 16)), dim3(256), 0, s, c->view, m.st,
-                       reinterpret_cast<const uint8_t *>(m.keys), m.rank, epoch);
+                       reinterpret_cast<const uint8_t *>(m.keys), m.rank, epoch, m.cap);
     rc = launch_status();
   }
   unsigned long long host = 0;
   if (rc == KVGOV_OK && out &&
       hipMemcpyAsync(&host, count, sizeof host, hipMemcpyDeviceToHost, s) != hipSuccess)
     rc = KVGOV_E_HIP;
-  if (hipFreeAsync(m.base, s) != hipSuccess && rc == KVGOV_OK) rc = KVGOV_E_HIP;
+  if (m.lk.owns_lock()) m.lk.unlock();  // everything that uses the scratch is enqueued
   if (rc == KVGOV_OK && out) {
     if (hipStreamSynchronize(s) != hipSuccess) return KVGOV_E_HIP;
     *out = (int64_t)host;

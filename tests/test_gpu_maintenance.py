@@ -236,3 +236,56 @@ def test_clear_resets_recency_of_a_tracked_table():
             assert key_set(c.export()) == {a[i].tobytes() for i in (1, 2)}
             c.clear()
             assert c.count() == 0
+
+
+def test_concurrent_maintenance_on_two_streams():
+    """Two tables, each on a stream of its own, run their inserts, eviction
+    and erase at the same time (every call asynchronous), three times over
+    with a clear before each round, as the two modes of the maintenance
+    bench step do; then each table holds what the oracle's does and answers
+    lookups the same way."""
+    g = np.random.default_rng(11)
+    jobs = []
+    for t in range(2):
+        lens = g.integers(1, 80, 3000)
+        keys = g.integers(0, 256, (int(lens.sum()), 32), dtype=np.uint8)
+        keys[:, 0] = 9 + t  # distinct per table, never the all-0xFF key
+        keys[:, 1] = 0
+        bo = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+        half = int(bo[1500])
+        a = (keys[:half], bo[:1501])
+        b = (keys[half:], bo[1500:] - half)
+        T = O.Table()
+        T.insert(*a)
+        T.insert(*b)
+        max_keys = len(T.keys) // 2
+        T.evict(max_keys)
+        erase = keys[:half // 10]
+        T.erase(erase)
+        jobs.append(dict(a=a, b=b, max_keys=max_keys, erase=erase, T=T, keys=keys, bo=bo))
+    streams = [torch.cuda.Stream() for _ in jobs]
+    caches = [KV.Cache(18) for _ in jobs]
+    try:
+        dj = []
+        for j in jobs:
+            dj.append(dict(a=(dev(j["a"][0]), dev(j["a"][1])), b=(dev(j["b"][0]), dev(j["b"][1])),
+                           erase=dev(j["erase"]), keys=dev(j["keys"]), bo=dev(j["bo"])))
+        for c in caches:
+            c.set_recency(True)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            for j, d, c, s in zip(jobs, dj, caches, streams):
+                c.clear(stream=s)
+                c.insert(*d["a"], sync=False, stream=s)
+                c.insert(*d["b"], sync=False, stream=s)
+                c.evict(j["max_keys"], sync=False, stream=s)
+                c.erase(d["erase"], sync=False, stream=s)
+        torch.cuda.synchronize()
+        for j, d, c in zip(jobs, dj, caches):
+            assert c.count() == len(j["T"].keys)
+            assert key_set(c.export()) == j["T"].keys
+            hits = c.lookup(d["keys"], d["bo"]).cpu().numpy()
+            assert np.array_equal(hits, j["T"].lookup(j["keys"], j["bo"]))
+    finally:
+        for c in caches:
+            c.close()
