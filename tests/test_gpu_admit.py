@@ -178,3 +178,50 @@ def test_admit_table_full_latched():
         with pytest.raises(K.KvgovError) as e:
             c.admit(hk, dev(np.array([0, 25, 40], np.int64)))
         assert e.value.code == c_["KVGOV_E_FULL"]
+
+
+def test_concurrent_admission_on_two_streams():
+    """Two tables, each on a stream of its own, admit different batches at
+    the same time (the per-row codes live in each stream's scratch), three
+    rounds with a clear before each, every call asynchronous; each round's
+    hits and new blocks equal the oracle's."""
+    g = np.random.default_rng(23)
+    jobs = []
+    for t in range(2):
+        fam = g.integers(0, 256, (40, 120, 32), dtype=np.uint8)
+        fam[:, :, 0] = 3 + t
+        rows, lens = [], []
+        for r in range(2500):
+            L = int(g.integers(0, 120))
+            k = g.integers(0, 256, (L, 32), dtype=np.uint8)
+            s_ = int(g.integers(0, L + 1))
+            k[:s_] = fam[int(g.integers(0, 40)), :s_]
+            rows.append(k)
+            lens.append(L)
+        h = np.concatenate(rows)
+        bo = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+        wh, wn = O.Table().admit(h, bo)
+        jobs.append(dict(h=h, bo=bo, wh=wh, wn=wn))
+    streams = [torch.cuda.Stream() for _ in jobs]
+    caches = [K.Cache(18) for _ in jobs]
+    try:
+        dj = [dict(h=dev(j["h"]), bo=dev(j["bo"]),
+                   hits=[torch.empty(j["bo"].size - 1, dtype=torch.int32, device="cuda")
+                         for _ in range(3)],
+                   new=[torch.empty(j["bo"].size - 1, dtype=torch.int32, device="cuda")
+                        for _ in range(3)]) for j in jobs]
+        torch.cuda.synchronize()
+        for rnd in range(3):
+            for d, c, s in zip(dj, caches, streams):
+                c.clear(stream=s)
+                c.admit(d["h"], d["bo"], sync=False, hits=d["hits"][rnd], new=d["new"][rnd],
+                        stream=s)
+        torch.cuda.synchronize()
+        for j, d, c in zip(jobs, dj, caches):
+            for rnd in range(3):
+                assert np.array_equal(d["hits"][rnd].cpu().numpy(), j["wh"])
+                assert np.array_equal(d["new"][rnd].cpu().numpy(), j["wn"])
+            assert c.count() == int(j["wn"].sum())
+    finally:
+        for c in caches:
+            c.close()
